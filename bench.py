@@ -1,0 +1,168 @@
+"""Benchmark: Lloyd iterations per second of exact k-means on one MI355X.
+
+Workload: N = 8,388,608 points, D = 128, K = 4,096 centroids, bf16 points with
+fp32 accumulation and fp32 centroids, a Zipf(1.1)-weighted Gaussian mixture
+(the synthetic stand-in for the paper's token embeddings).  One step = one
+Lloyd iteration (assignment + centroid update) through ``kmeans_lloyd``.
+
+Prints one JSON line with the metric, a roofline object for the dominant
+kernel (assignment: 2 N K D flops per launch against the dense bf16 MFMA peak)
+and the fp64 CPU oracle's rate on the host cores as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Lloyd iter/s; assign TFLOP/s as % of MFMA peak at N=8M D=128 K=4096"
+PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16 MFMA (no sparsity)
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "assign_traffic.json")
+ASSIGN_SRC = os.path.join(ROOT, "paper_2608_12629_amd", "csrc", "assign.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    with open(ASSIGN_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def stored_traffic():
+    """Measured HBM bytes per assignment launch, if taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return rec.get("bytes_per_launch") if rec.get("kernel_sha256_16") == kernel_hash() else None
+
+
+def cpu_baseline(w, sample_rows: int):
+    """The fp64 oracle on the host: one Lloyd iteration, assignment timed on a row sample."""
+    import numpy as np
+    from oracle import default
+    from paper_2608_12629_amd.synth import raw_bits
+
+    o = default()
+    xr = raw_bits(w.X)
+    C64 = w.C0.double().numpy()
+    rows = np.ascontiguousarray(xr[:, :sample_rows])
+    t0 = time.perf_counter()
+    idx_s, _, _ = o.assign(rows, w.dtype, C64)
+    t_assign = time.perf_counter() - t0
+    # the update is O(N D): time it in full, on an assignment of every point
+    idx_full = np.resize(idx_s, (w.B, w.N)).astype(np.int32)
+    t0 = time.perf_counter()
+    o.update(xr, w.dtype, idx_full, C64)
+    t_update = time.perf_counter() - t0
+    t_iter = t_assign * (w.N / sample_rows) + t_update
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": 1.0 / t_iter, "unit": "iter/s", "cores": cores, "kind": "oracle",
+            "sample": f"assignment of the first {sample_rows} of {w.N} points against all "
+                      f"{w.K} centroids ({t_assign:.2f} s, scaled by N/{sample_rows}) + the "
+                      f"full update ({t_update:.2f} s); fp64, OpenMP"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--kernel-reps", type=int, default=10)
+    ap.add_argument("--cpu-sample", type=int, default=65536)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(rerun with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_12629_amd import kmeans as km
+    from paper_2608_12629_amd.synth import make_workload
+
+    t0 = time.perf_counter()
+    w = make_workload(3)
+    log(f"workload {w.name} generated in {time.perf_counter() - t0:.1f} s")
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    X = w.X.to(dev)
+    C0 = w.C0.to(dev)
+    B, N, D, K = w.B, w.N, w.D, w.K
+    ws = km.Workspace(B, N, D, K, X.dtype, dev)
+    C = C0.clone()
+    idx = torch.empty((B, N), dtype=torch.int32, device=dev)
+    md = torch.empty((B, N), dtype=torch.float32, device=dev)
+    cnt = torch.empty((B, K), dtype=torch.int32, device=dev)
+
+    # warm-up, then exactly `steps` Lloyd iterations from C0
+    km.kmeans_lloyd(X, C, args.warmup, idx=idx, min_dist=md, counts=cnt, ws=ws)
+    C.copy_(C0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    km.kmeans_lloyd(X, C, args.steps, idx=idx, min_dist=md, counts=cnt, ws=ws)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    log(f"{args.steps} Lloyd iterations in {dt * 1e3:.2f} ms")
+
+    # per-kernel durations with HIP events on the stream the library launches on
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ev[0].record(stream)
+    for _ in range(args.kernel_reps):
+        km.kmeans_assign(X, C0, idx=idx, min_dist=md, ws=ws)
+    ev[1].record(stream)
+    for _ in range(args.kernel_reps):
+        km.kmeans_update(X, idx, C0, C_out=C, counts=cnt, ws=ws)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    assign_ms = ev[0].elapsed_time(ev[1]) / args.kernel_reps
+    update_ms = ev[1].elapsed_time(ev[2]) / args.kernel_reps
+    flops = 2.0 * B * N * K * D
+    assign_tflops = flops / (assign_ms * 1e-3) / 1e12
+    upd_bytes = B * N * D * X.element_size() + 4 * B * N + 4 * B * K * D + 4 * B * K
+    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9
+    log(f"assign {assign_ms:.3f} ms = {assign_tflops:.1f} TFLOP/s; "
+        f"update {update_ms:.3f} ms = {upd_gbs:.0f} GB/s algorithmic")
+
+    out = {
+        "metric": METRIC,
+        "value": args.steps / dt,
+        "unit": "iter/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "N": N, "D": D, "K": K, "x_dtype": "bf16",
+                   "centroid_dtype": "f32", "iters_per_step": 1},
+        "roofline": {"bound": "mfma", "kernel": "assign", "achieved": assign_tflops,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": assign_tflops / PEAK_BF16_TFLOPS, "traffic": stored_traffic()},
+        "update": {"ms": update_ms, "algorithmic_bytes": upd_bytes, "GB/s": upd_gbs,
+                   "hbm_frac": upd_gbs / PEAK_HBM_GBS},
+        "assign_ms": assign_ms,
+    }
+    if not args.no_cpu:
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample)
+        log(f"cpu baseline in {time.perf_counter() - t0:.1f} s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

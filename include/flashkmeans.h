@@ -1,0 +1,115 @@
+/*
+ * flashkmeans.h -- C ABI of libflashkmeans.so: the exact k-means (Lloyd)
+ * iteration on AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow the Flash-KMeans workload of the paper (Section 5,
+ * "Flash-KMeans clean-start workload"): a Lloyd iteration is an assignment
+ * step (squared Euclidean distance of every point to every centroid, then an
+ * arg-min) and a centroid update (per-cluster sums and counts of the points,
+ * then their quotient).  B independent instances may be processed in one call.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All array arguments are DEVICE pointers to row-major, contiguous arrays,
+ *   16-byte aligned.  The caller owns all memory; the library allocates
+ *   nothing and keeps no state except a per-device architecture check.
+ * - X holds B instances of N points of D dimensions: [B, N, D] in the storage
+ *   type `xdtype` (FKM_F32, FKM_BF16 or FKM_F16).
+ * - Centroids are fp32: [B, K, D].  The assignment rounds them once to the
+ *   storage type (round-to-nearest-even) to feed the matrix cores and uses the
+ *   squared norm of the rounded centroid, so each distance is the distance to
+ *   that rounded centroid, accumulated in fp32.
+ * - Indices are int32 and local to an instance: idx[b, i] is in [0, K).
+ * - Ties go to the lowest centroid index.  An empty cluster keeps its previous
+ *   centroid (and reports count 0).
+ * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *   the call returns without synchronizing.  Results are deterministic:
+ *   identical inputs give bit-identical outputs.
+ * - `ws` is a device workspace of at least kmeans_workspace_bytes(...) bytes.
+ *   Its contents are scratch; calls that share a workspace must be ordered on
+ *   one stream.
+ * - Errors: arguments are validated on the host before anything is enqueued;
+ *   a rejected call returns a negative status and has no effect.
+ *   FKM_ERR_UNSUPPORTED means valid but outside what this build implements
+ *   (not gfx950, D not a multiple of 32, D > 2048, K > 32768, N > 2^31-1).
+ *   FKM_ERR_HIP reports a failed HIP call or launch.  No C++ exception
+ *   crosses this boundary.
+ */
+#ifndef FLASHKMEANS_H_
+#define FLASHKMEANS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { FKM_F32 = 0, FKM_BF16 = 1, FKM_F16 = 2 } fkm_dtype;
+
+typedef enum {
+    FKM_OK = 0,
+    FKM_ERR_INVALID_ARG = -1,  /* null pointer, size < 1, bad dtype, misaligned pointer, iters < 1 */
+    FKM_ERR_UNSUPPORTED = -2,  /* see the limits above */
+    FKM_ERR_WORKSPACE = -3,    /* ws NULL or ws_bytes smaller than kmeans_workspace_bytes() */
+    FKM_ERR_HIP = -4           /* a HIP runtime call or a kernel launch failed */
+} fkm_status;
+
+/*
+ * Bytes of device workspace that kmeans_assign, kmeans_update and
+ * kmeans_lloyd need for these sizes (one size serves all three).  Returns 0
+ * for arguments that those calls would reject.  Pure host arithmetic.
+ */
+size_t kmeans_workspace_bytes(int64_t B, int64_t N, int64_t D, int64_t K, int xdtype);
+
+/*
+ * Assignment step (paper Section 5: distances from each point to all K
+ * centroids, then the arg-min).  The N x K distance matrix is never stored.
+ *   X        [B, N, D] xdtype   points (read)
+ *   C        [B, K, D] fp32     centroids (read)
+ *   idx      [B, N]    int32    written: lowest k minimising ||x - c_k||^2
+ *   min_dist [B, N]    fp32     written: that squared distance, clamped at 0
+ */
+int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t N, int64_t D,
+                  int64_t K, int32_t* idx, float* min_dist, void* ws, size_t ws_bytes,
+                  void* stream);
+
+/*
+ * Centroid update (paper Section 5: reduce the points of each cluster into a
+ * per-cluster sum and count).  The reduction is a counting sort of the point
+ * ids by cluster followed by a segmented sum in fp32 in a fixed order; no
+ * floating-point atomics are used.
+ *   X       [B, N, D] xdtype  points (read)
+ *   idx     [B, N]    int32   cluster of each point (read); a value outside
+ *                             [0, K) excludes that point from every count and sum
+ *   C_prev  [B, K, D] fp32    previous centroids; rows of empty clusters are
+ *                             copied to C_out (read)
+ *   C_out   [B, K, D] fp32    written: sum_k / count_k (IEEE fp32 division);
+ *                             may alias C_prev
+ *   counts  [B, K]    int32   written: count_k
+ */
+int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_prev, int64_t B,
+                  int64_t N, int64_t D, int64_t K, float* C_out, int32_t* counts, void* ws,
+                  size_t ws_bytes, void* stream);
+
+/*
+ * `iters` Lloyd iterations (assignment then update), all enqueued on stream.
+ *   C         [B, K, D] fp32   in: C_0, out: C_iters (updated in place)
+ *   idx       [B, N]    int32  written: assignment of the last iteration
+ *   min_dist  [B, N]    fp32   written: distances of the last iteration
+ *   counts    [B, K]    int32  written: cluster sizes of the last iteration
+ *   objective [B, iters] fp64  written if not NULL: J_t = sum_i min_dist_i of
+ *                              the assignment made under C_t, summed in fp64
+ */
+int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D, int64_t K,
+                 int iters, int32_t* idx, float* min_dist, int32_t* counts, double* objective,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* kmeans_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHKMEANS_H_ */

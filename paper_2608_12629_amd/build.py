@@ -1,0 +1,38 @@
+"""Build ``libflashkmeans.so`` (gfx950 only) from the HIP sources in ``csrc/``.
+
+``python -m paper_2608_12629_amd.build`` or ``build()``; the library is written
+next to this file, where ``paper_2608_12629_amd.kmeans`` loads it.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libflashkmeans.so")
+SOURCES = ["api.hip", "assign.hip", "update.hip"]
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+FLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    # packed fp32 instructions are not emitted (see the design notes)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+
+
+def build(out: str = LIB, extra=()) -> str:
+    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    tmp = out + f".tmp{os.getpid()}"
+    cmd = [HIPCC, *FLAGS, *extra, *srcs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{r.stderr[-6000:]}")
+    os.replace(tmp, out)
+    return out
+
+
+if __name__ == "__main__":
+    print(build(*sys.argv[1:2]))

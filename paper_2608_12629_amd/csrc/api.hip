@@ -1,0 +1,156 @@
+// api.hip -- the C ABI of libflashkmeans.so (declared in include/flashkmeans.h):
+// host-side argument validation, workspace carving, the gfx950 check and the
+// launch sequence of each entry point.  Nothing here touches the GPU before
+// the arguments have been validated.
+#include <atomic>
+#include <cstring>
+
+#include "../../include/flashkmeans.h"
+#include "fkm_internal.h"
+
+namespace fkm {
+
+static size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
+
+Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
+  Workspace w{};
+  w.n_assign_blocks = (N + assign_points_per_block(dt, (int)D) - 1) / assign_points_per_block(dt, (int)D);
+  w.n_sort_chunks = (N + SORT_WC - 1) / SORT_WC;
+  w.n_seg = (w.n_sort_chunks + SORT_SEG - 1) / SORT_SEG;
+  w.n_red_chunks = (N + RED_CR - 1) / RED_CR;
+  char* p = (char*)base;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    char* r = p ? p + o : nullptr;
+    o = align_up(o + bytes);
+    return r;
+  };
+  w.chat = take((size_t)(B * K * D) * dt_bytes(dt));
+  w.cinit = (float*)take((size_t)(B * K) * 4);
+  w.objpart = (double*)take((size_t)(B * w.n_assign_blocks) * 8);
+  w.hist = (int32_t*)take((size_t)(B * w.n_sort_chunks * K) * 4);
+  w.segsum = (int32_t*)take((size_t)(B * w.n_seg * K) * 4);
+  w.off = (int32_t*)take((size_t)(B * (K + 1)) * 4);
+  w.perm = (int32_t*)take((size_t)(B * N) * 4);
+  w.carry = (float*)take((size_t)(B * w.n_red_chunks * 2 * D) * 4);
+  w.sums = (float*)take((size_t)(B * K * D) * 4);
+  w.total = o;
+  return w;
+}
+
+// ---- validation --------------------------------------------------------------
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+static int check_sizes(int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
+  if (B < 1 || N < 1 || D < 1 || K < 1) return FKM_ERR_INVALID_ARG;
+  if (dt != DT_F32 && dt != DT_BF16 && dt != DT_F16) return FKM_ERR_INVALID_ARG;
+  if (N > INT32_MAX || K > MAX_K || D > MAX_D || B > 65535) return FKM_ERR_UNSUPPORTED;
+  if (!row_bytes_ok(dt, D) || !assign_resident_ok(dt, D)) return FKM_ERR_UNSUPPORTED;
+  return FKM_OK;
+}
+
+static int check_ptrs(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!p || !aligned16(p)) return FKM_ERR_INVALID_ARG;
+  return FKM_OK;
+}
+
+static int check_ws(void* ws, size_t ws_bytes, int64_t B, int64_t N, int64_t D, int64_t K,
+                    int dt) {
+  if (!ws || !aligned16(ws)) return FKM_ERR_WORKSPACE;
+  if (ws_bytes < carve(nullptr, B, N, D, K, dt).total) return FKM_ERR_WORKSPACE;
+  return FKM_OK;
+}
+
+// 0 = not checked yet, 1 = gfx950, 2 = other device
+static std::atomic<int> g_arch[256];
+
+static int check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FKM_ERR_HIP;
+  if (dev < 0 || dev >= 256) return FKM_ERR_UNSUPPORTED;
+  int st = g_arch[dev].load(std::memory_order_acquire);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return FKM_ERR_HIP;
+    st = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    if (st == 1 && update_init() != hipSuccess) return FKM_ERR_HIP;
+    g_arch[dev].store(st, std::memory_order_release);
+  }
+  return st == 1 ? FKM_OK : FKM_ERR_UNSUPPORTED;
+}
+
+static int hip_status(hipError_t e) { return e == hipSuccess ? FKM_OK : FKM_ERR_HIP; }
+
+}  // namespace fkm
+
+using namespace fkm;
+
+extern "C" {
+
+size_t kmeans_workspace_bytes(int64_t B, int64_t N, int64_t D, int64_t K, int xdtype) {
+  if (check_sizes(B, N, D, K, xdtype) != FKM_OK) return 0;
+  return carve(nullptr, B, N, D, K, xdtype).total;
+}
+
+int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t N, int64_t D,
+                  int64_t K, int32_t* idx, float* min_dist, void* ws, size_t ws_bytes,
+                  void* stream) {
+  int rc;
+  if ((rc = check_ptrs({X, C, idx, min_dist}))) return rc;
+  if ((rc = check_sizes(B, N, D, K, xdtype))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, B, N, D, K, xdtype))) return rc;
+  if ((rc = check_device())) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  const Workspace w = carve(ws, B, N, D, K, xdtype);
+  if ((rc = hip_status(launch_prep(C, xdtype, B * K, D, w.chat, w.cinit, s)))) return rc;
+  return hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s));
+}
+
+int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_prev, int64_t B,
+                  int64_t N, int64_t D, int64_t K, float* C_out, int32_t* counts, void* ws,
+                  size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_ptrs({X, idx, C_prev, C_out, counts}))) return rc;
+  if ((rc = check_sizes(B, N, D, K, xdtype))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, B, N, D, K, xdtype))) return rc;
+  if ((rc = check_device())) return rc;
+  const Workspace w = carve(ws, B, N, D, K, xdtype);
+  return hip_status(launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts,
+                                  (hipStream_t)stream));
+}
+
+int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D, int64_t K,
+                 int iters, int32_t* idx, float* min_dist, int32_t* counts, double* objective,
+                 void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_ptrs({X, C, idx, min_dist, counts}))) return rc;
+  if (objective && !aligned16(objective)) return FKM_ERR_INVALID_ARG;
+  if (iters < 1) return FKM_ERR_INVALID_ARG;
+  if ((rc = check_sizes(B, N, D, K, xdtype))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, B, N, D, K, xdtype))) return rc;
+  if ((rc = check_device())) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  const Workspace w = carve(ws, B, N, D, K, xdtype);
+  for (int t = 0; t < iters; ++t) {
+    if ((rc = hip_status(launch_prep(C, xdtype, B * K, D, w.chat, w.cinit, s)))) return rc;
+    if ((rc = hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s)))) return rc;
+    if (objective && (rc = hip_status(launch_objective(w, B, iters, t, objective, s)))) return rc;
+    if ((rc = hip_status(launch_update(X, xdtype, idx, C, w, B, N, D, K, C, counts, s))))
+      return rc;
+  }
+  return FKM_OK;
+}
+
+const char* kmeans_status_string(int status) {
+  switch (status) {
+    case FKM_OK: return "ok";
+    case FKM_ERR_INVALID_ARG: return "invalid argument";
+    case FKM_ERR_UNSUPPORTED: return "unsupported (device or shape outside this build)";
+    case FKM_ERR_WORKSPACE: return "workspace missing or too small";
+    case FKM_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,328 @@
+// assign.hip -- the assignment step of the Lloyd iteration (paper Section 5:
+// squared Euclidean distance of each point to all K centroids, then the
+// arg-min), fused so that the N x K distance matrix is never stored.
+//
+// For point x and centroid c the kernel maximises
+//     s(x, c) = <x, c^> - |c^|^2 / 2
+// which orders the centroids exactly as |x - c^|^2 = |x|^2 - 2 s(x, c) does
+// (|x|^2 is common to all of them).  c^ is the centroid rounded once to the
+// storage type of x; <x, c^> runs on the matrix cores (bf16/fp16 16x16x32 or
+// fp32 16x16x4 MFMA) with fp32 accumulation, and -|c^|^2 / 2 enters as the
+// accumulator's initial value, so the epilogue is a bare compare-and-select.
+//
+// Layout of one MFMA tile: 16 centroids (A rows) x 16 points (B columns).
+// Lane l = 16 g + m supplies centroid row m and point column m for the
+// k-slice g (the k-to-lane map is the same for A and B, so any fixed split of
+// the D dimensions over the four lane groups gives the same contraction);
+// it receives accumulator rows 4 g .. 4 g + 3 of column m.  A lane therefore
+// keeps a running best over its own quarter of the centroids of one point,
+// and the four quarters are merged once at the end.
+#include "fkm_internal.h"
+
+namespace fkm {
+
+// ---------------------------------------------------------------------------
+// element helpers
+template <int DT> struct Elem;
+template <> struct Elem<DT_BF16> {
+  static constexpr int per16 = 8;  // elements in 16 bytes
+  __device__ static float widen(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+  __device__ static uint16_t narrow(float f) {
+    __bf16 b = (__bf16)f;  // round to nearest even
+    return __builtin_bit_cast(uint16_t, b);
+  }
+};
+template <> struct Elem<DT_F16> {
+  static constexpr int per16 = 8;
+  __device__ static float widen(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+  __device__ static uint16_t narrow(float f) {
+    _Float16 b = (_Float16)f;  // round to nearest even
+    return __builtin_bit_cast(uint16_t, b);
+  }
+};
+template <> struct Elem<DT_F32> {
+  static constexpr int per16 = 4;
+};
+
+// Sum of squares of the elements of one 16-byte chunk, widened to fp32,
+// accumulated in element order.
+template <int DT>
+__device__ inline float chunk_sumsq(const uint4& q, float acc) {
+  if constexpr (DT == DT_F32) {
+    const float v[4] = {__uint_as_float(q.x), __uint_as_float(q.y), __uint_as_float(q.z),
+                        __uint_as_float(q.w)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = __builtin_fmaf(v[e], v[e], acc);
+  } else {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = Elem<DT>::widen((uint16_t)(w[e] & 0xffffu));
+      const float hi = Elem<DT>::widen((uint16_t)(w[e] >> 16));
+      acc = __builtin_fmaf(lo, lo, acc);
+      acc = __builtin_fmaf(hi, hi, acc);
+    }
+  }
+  return acc;
+}
+
+// acc += A-chunk x B-chunk over the k-slice these two 16-byte chunks carry.
+template <int DT>
+__device__ inline f32x4 mfma_chunk(const uint4& a, const uint4& b, f32x4 acc) {
+  if constexpr (DT == DT_BF16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  } else if constexpr (DT == DT_F16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+  } else {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    return acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// prep: c^ = round(c) to the storage type and cinit = -|c^|^2 / 2 (fp32),
+// one wave per centroid row; the squared norm is summed lane-strided and then
+// by a fixed xor butterfly, so every lane (and every call) gets the same bits.
+template <int DT>
+__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, int64_t rows,
+                                                   int D, void* __restrict__ chat,
+                                                   float* __restrict__ cinit) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float* c = C + row * D;
+  float ss = 0.f;
+  if constexpr (DT == DT_F32) {
+    float* out = (float*)chat + row * D;
+    for (int d = lane; d < D; d += 64) {
+      const float v = c[d];
+      out[d] = v;
+      ss = __builtin_fmaf(v, v, ss);
+    }
+  } else {
+    uint16_t* out = (uint16_t*)chat + row * D;
+    for (int d = lane; d < D; d += 64) {
+      const uint16_t h = Elem<DT>::narrow(c[d]);
+      out[d] = h;
+      const float v = Elem<DT>::widen(h);
+      ss = __builtin_fmaf(v, v, ss);
+    }
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
+  if (lane == 0) cinit[row] = -0.5f * ss;
+}
+
+// ---------------------------------------------------------------------------
+// Resident-X assignment.  CPL = 16-byte chunks of one point held by one lane
+// (the point's row is split over the four lane groups), NSUB = 16-point MFMA
+// column tiles per wave.
+template <int DT, int CPL, int NSUB>
+__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
+    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
+    int N, int K, int32_t* __restrict__ idx, float* __restrict__ min_dist,
+    double* __restrict__ objpart) {
+  constexpr int RC = 4 * CPL;              // 16-byte chunks per row
+  constexpr int SWZ = RC < 16 ? RC - 1 : 15;
+  constexpr int TCS = ASSIGN_TCS;
+  constexpr int PPW = 16 * NSUB;           // points per wave
+  constexpr int PPB = 4 * PPW;             // points per workgroup
+  constexpr int LOADS = TCS * RC / ASSIGN_THREADS;  // chunks per thread per stage
+  static_assert(LOADS * ASSIGN_THREADS == TCS * RC, "stage must split evenly");
+
+  __shared__ uint4 lds_c[2][TCS * RC];
+  __shared__ __attribute__((aligned(16))) float lds_n[2][TCS];
+  __shared__ double lds_obj[4];
+
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  X += (size_t)b * N * RC;
+  chat += (size_t)b * K * RC;
+  cinit += (size_t)b * K;
+  idx += (size_t)b * N;
+  min_dist += (size_t)b * N;
+
+  // ---- this lane's slices of its NSUB points, and their squared norms
+  const int pbase = blockIdx.x * PPB + wave * PPW;
+  uint4 xr[NSUB][CPL];
+  float xn[NSUB];
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    const int pt = pbase + p * 16 + m;
+    const bool ok = pt < N;
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      xr[p][c] = ok ? X[(size_t)pt * RC + g * CPL + c] : make_uint4(0, 0, 0, 0);
+      ss = chunk_sumsq<DT>(xr[p][c], ss);
+    }
+    ss += __shfl_xor(ss, 16);
+    ss += __shfl_xor(ss, 32);
+    xn[p] = ss;
+  }
+
+  // ---- centroid stages through LDS (double-buffered)
+  const int nst = (K + TCS - 1) / TCS;
+  uint4 pre[LOADS];
+  float pren = 0.f;
+  auto load_stage = [&](int st) {
+    const int kb = st * TCS;
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int q = tid + u * ASSIGN_THREADS;
+      const int r = q / RC, c = q % RC;
+      pre[u] = (kb + r < K) ? chat[(size_t)(kb + r) * RC + c] : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < TCS) pren = (kb + tid < K) ? cinit[kb + tid] : -__builtin_inff();
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int q = tid + u * ASSIGN_THREADS;
+      const int r = q / RC, c = q % RC;
+      lds_c[buf][r * RC + (c ^ (r & SWZ))] = pre[u];
+    }
+    if (tid < TCS) lds_n[buf][tid] = pren;
+  };
+
+  float best[NSUB];
+  int code[NSUB];
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    best[p] = -__builtin_inff();
+    code[p] = 0;
+  }
+
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nst) load_stage(st + 1);
+#pragma unroll 1
+    for (int tile = 0; tile < TCS / 16; ++tile) {
+      const int row = tile * 16 + m;
+      const f32x4 cin = *reinterpret_cast<const f32x4*>(&lds_n[buf][tile * 16 + 4 * g]);
+      uint4 a[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) a[c] = lds_c[buf][row * RC + ((g * CPL + c) ^ (row & SWZ))];
+      const int kcode = st * TCS + tile * 16;  // + 4 g + j is the centroid index
+#pragma unroll
+      for (int p = 0; p < NSUB; ++p) {
+        f32x4 acc = cin;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) acc = mfma_chunk<DT>(a[c], xr[p][c], acc);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bool gt = acc[j] > best[p];
+          best[p] = gt ? acc[j] : best[p];
+          code[p] = gt ? kcode + j : code[p];
+        }
+      }
+    }
+    if (st + 1 < nst) store_stage(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- merge the four centroid quarters of each point; ties -> lower index
+  double obj = 0.0;
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    float v = best[p];
+    int i = code[p] + 4 * g;
+#pragma unroll
+    for (int msk = 16; msk <= 32; msk <<= 1) {
+      const float vo = __shfl_xor(v, msk);
+      const int io = __shfl_xor(i, msk);
+      const bool take = (vo > v) || (vo == v && io < i);
+      v = take ? vo : v;
+      i = take ? io : i;
+    }
+    const int pt = pbase + p * 16 + m;
+    if (g == 0 && pt < N) {
+      const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v, xn[p]), 0.f);
+      idx[pt] = i;
+      min_dist[pt] = md;
+      obj += (double)md;
+    }
+  }
+#pragma unroll
+  for (int msk = 1; msk < 64; msk <<= 1) obj += __shfl_xor(obj, msk);
+  if (lane == 0) lds_obj[wave] = obj;
+  __syncthreads();
+  if (tid == 0)
+    objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
+}
+
+// Sum of one instance's workgroup partials in a fixed order, in fp64.
+__global__ __launch_bounds__(256) void objective_kernel(const double* __restrict__ part, int nblk,
+                                                        int iters, int t, double* __restrict__ out) {
+  __shared__ double s[256];
+  const int b = blockIdx.x;
+  double a = 0.0;
+  for (int i = threadIdx.x; i < nblk; i += 256) a += part[(size_t)b * nblk + i];
+  s[threadIdx.x] = a;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[(size_t)b * iters + t] = s[0];
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_prep(const float* C, int dt, int64_t rows, int64_t D, void* chat, float* cinit,
+                       hipStream_t s) {
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (dt == DT_BF16) prep_kernel<DT_BF16><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
+  else if (dt == DT_F16) prep_kernel<DT_F16><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
+  else prep_kernel<DT_F32><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
+  return hipGetLastError();
+}
+
+template <int DT, int CPL>
+static hipError_t launch_resident(const void* X, const Workspace& w, int64_t B, int64_t N,
+                                  int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
+  constexpr int NSUB = CPL <= 4 ? 8 : 4;
+  const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
+  assign_resident_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
+      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)K, idx, min_dist, w.objpart);
+  return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t launch_resident_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
+                                     int64_t D, int64_t K, int32_t* idx, float* min_dist,
+                                     hipStream_t s) {
+  switch (D * dt_bytes(DT) / 64) {
+    case 1: return launch_resident<DT, 1>(X, w, B, N, K, idx, min_dist, s);
+    case 2: return launch_resident<DT, 2>(X, w, B, N, K, idx, min_dist, s);
+    case 4: return launch_resident<DT, 4>(X, w, B, N, K, idx, min_dist, s);
+    case 8: return launch_resident<DT, 8>(X, w, B, N, K, idx, min_dist, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
+                         int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
+  if (!assign_resident_ok(dt, D)) return hipErrorInvalidValue;
+  if (dt == DT_BF16) return launch_resident_dt<DT_BF16>(X, w, B, N, D, K, idx, min_dist, s);
+  if (dt == DT_F16) return launch_resident_dt<DT_F16>(X, w, B, N, D, K, idx, min_dist, s);
+  return launch_resident_dt<DT_F32>(X, w, B, N, D, K, idx, min_dist, s);
+}
+
+hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
+                            hipStream_t s) {
+  objective_kernel<<<dim3((unsigned)B), dim3(256), 0, s>>>(w.objpart, (int)w.n_assign_blocks,
+                                                           iters, t, objective);
+  return hipGetLastError();
+}
+
+}  // namespace fkm

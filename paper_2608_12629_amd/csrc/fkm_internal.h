@@ -1,0 +1,84 @@
+// fkm_internal.h -- types, tuning constants and launcher declarations shared by
+// the HIP translation units of libflashkmeans.so.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fkm {
+
+enum Dt { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
+
+inline int dt_bytes(int dt) { return dt == DT_F32 ? 4 : 2; }
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---- tuning constants -------------------------------------------------------
+// Assignment (resident-X kernel): 256 threads = 4 waves per workgroup; each
+// wave keeps ASSIGN_NSUB x 16 points in registers; centroids stream through
+// LDS in stages of ASSIGN_TCS rows.
+constexpr int ASSIGN_THREADS = 256;
+constexpr int ASSIGN_TCS = 64;
+// Update: the counting sort works on chunks of SORT_WC points (one wave ranks
+// a chunk); chunk histograms are scanned in segments of SORT_SEG chunks; the
+// segmented sum gives each wave RED_CR consecutive entries of the sorted order.
+constexpr int SORT_WC = 4096;
+constexpr int SORT_SEG = 32;
+constexpr int RED_CR = 2048;
+// Limits of this build.
+constexpr int64_t MAX_K = 32768;   // LDS counters of the counting sort
+constexpr int64_t MAX_D = 2048;
+
+// Row widths (bytes per point) the kernels handle: a power of two from 64 B
+// (16 bf16/fp16 or 16 fp32 values would be 32/64 B; D % 32 == 0 is required)
+// up to 8 KiB.
+inline bool row_bytes_ok(int dt, int64_t D) {
+  const int64_t rb = D * dt_bytes(dt);
+  return D % 32 == 0 && rb >= 64 && rb <= 8192 && (rb & (rb - 1)) == 0;
+}
+
+inline int assign_nsub(int dt, int D) {
+  const int cpl = D * dt_bytes(dt) / 64;  // 16-byte chunks per lane
+  return cpl <= 4 ? 8 : 4;
+}
+inline int64_t assign_points_per_block(int dt, int D) { return 64 * assign_nsub(dt, D); }
+
+// The resident-X assignment kernel handles these row widths (bytes per point).
+inline bool assign_resident_ok(int dt, int64_t D) {
+  const int64_t rb = D * dt_bytes(dt);
+  return rb == 64 || rb == 128 || rb == 256 || rb == 512;
+}
+
+// ---- workspace layout -------------------------------------------------------
+struct Workspace {
+  void* chat;      // [B,K,D] centroids rounded to the storage type
+  float* cinit;    // [B,K]   -1/2 * squared norm of each rounded centroid
+  double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
+  int32_t* hist;   // [B,n_sort_chunks,K] chunk histograms, then chunk start offsets
+  int32_t* segsum; // [B,n_seg,K] histogram sums per segment of chunks
+  int32_t* off;    // [B,K+1] cluster start offsets in the sorted order
+  int32_t* perm;   // [B,N] point ids sorted by cluster
+  float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by chunk ends
+  float* sums;     // [B,K,D] sums of clusters that fit in one chunk
+  int64_t n_assign_blocks, n_sort_chunks, n_seg, n_red_chunks;
+  size_t total;
+};
+
+Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt);
+
+// ---- launchers (return hipSuccess or the launch error) ----------------------
+hipError_t launch_prep(const float* C, int dt, int64_t rows, int64_t D, void* chat, float* cinit,
+                       hipStream_t s);
+hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
+                         int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
+                            hipStream_t s);
+hipError_t update_init();
+hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
+                         const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
+                         float* C_out, int32_t* counts, hipStream_t s);
+
+}  // namespace fkm

@@ -1,0 +1,172 @@
+"""ctypes binding of ``libflashkmeans.so`` (the C ABI in ``include/flashkmeans.h``).
+
+Argument marshalling only: every step of the Lloyd iteration runs in the HIP
+kernels of the library.  Tensors must be CUDA (HIP) tensors on the current
+device; work is enqueued on torch's current stream.  Importing this module
+raises if the library has not been built -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libflashkmeans.so")
+
+F32, BF16, F16 = 0, 1, 2
+_DTYPE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+
+
+class KMeansError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+        self.status = status
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2608_12629_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, vp, sz = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
+    lib.kmeans_workspace_bytes.argtypes = [i64, i64, i64, i64, i32]
+    lib.kmeans_workspace_bytes.restype = sz
+    lib.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
+    lib.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
+    lib.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
+    for f in (lib.kmeans_assign, lib.kmeans_update, lib.kmeans_lloyd):
+        f.restype = ctypes.c_int
+    lib.kmeans_status_string.argtypes = [ctypes.c_int]
+    lib.kmeans_status_string.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.kmeans_status_string(int(status)).decode()
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != OK:
+        raise KMeansError(rc, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _shapes(X: torch.Tensor, C: torch.Tensor) -> Tuple[int, int, int, int]:
+    if X.dim() == 2:
+        X = X.unsqueeze(0)
+    if C.dim() == 2:
+        C = C.unsqueeze(0)
+    if X.dim() != 3 or C.dim() != 3 or X.shape[0] != C.shape[0] or X.shape[2] != C.shape[2]:
+        raise ValueError(f"shapes X{tuple(X.shape)} C{tuple(C.shape)}: want [B,N,D] and [B,K,D]")
+    return X.shape[0], X.shape[1], X.shape[2], C.shape[1]
+
+
+def _dt(X: torch.Tensor) -> int:
+    try:
+        return _DTYPE[X.dtype]
+    except KeyError:
+        raise TypeError(f"points must be float32, bfloat16 or float16, got {X.dtype}") from None
+
+
+def _need(t: torch.Tensor, name: str, dtype=None) -> None:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def workspace_bytes(B: int, N: int, D: int, K: int, dtype: torch.dtype) -> int:
+    return int(lib.kmeans_workspace_bytes(B, N, D, K, _DTYPE[dtype]))
+
+
+class Workspace:
+    """A device buffer of ``kmeans_workspace_bytes`` bytes, reused across calls."""
+
+    def __init__(self, B: int, N: int, D: int, K: int, dtype: torch.dtype, device=None):
+        n = workspace_bytes(B, N, D, K, dtype)
+        if n == 0:
+            raise KMeansError(ERR_UNSUPPORTED, "kmeans_workspace_bytes")
+        self.nbytes = n
+        self.buf = torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def _ws(ws: Optional[Workspace], B, N, D, K, dtype, device) -> Workspace:
+    if ws is None or ws.nbytes < workspace_bytes(B, N, D, K, dtype):
+        ws = Workspace(B, N, D, K, dtype, device)
+    return ws
+
+
+def kmeans_assign(X: torch.Tensor, C: torch.Tensor, idx: Optional[torch.Tensor] = None,
+                  min_dist: Optional[torch.Tensor] = None, ws: Optional[Workspace] = None):
+    """idx, min_dist of the nearest centroid of every point (see ``kmeans_assign`` in the header)."""
+    B, N, D, K = _shapes(X, C)
+    _need(X, "X")
+    _need(C, "C", torch.float32)
+    idx = torch.empty((B, N), dtype=torch.int32, device=X.device) if idx is None else idx
+    min_dist = torch.empty((B, N), dtype=torch.float32, device=X.device) if min_dist is None else min_dist
+    _need(idx, "idx", torch.int32)
+    _need(min_dist, "min_dist", torch.float32)
+    ws = _ws(ws, B, N, D, K, X.dtype, X.device)
+    _check(lib.kmeans_assign(_ptr(X), _dt(X), _ptr(C), B, N, D, K, _ptr(idx), _ptr(min_dist),
+                             _ptr(ws.buf), ws.nbytes, _stream()), "kmeans_assign")
+    return idx, min_dist
+
+
+def kmeans_update(X: torch.Tensor, idx: torch.Tensor, C_prev: torch.Tensor,
+                  C_out: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
+                  ws: Optional[Workspace] = None):
+    """C_out, counts of the centroid update (see ``kmeans_update`` in the header)."""
+    B, N, D, K = _shapes(X, C_prev)
+    _need(X, "X")
+    _need(idx, "idx", torch.int32)
+    _need(C_prev, "C_prev", torch.float32)
+    C_out = torch.empty((B, K, D), dtype=torch.float32, device=X.device) if C_out is None else C_out
+    counts = torch.empty((B, K), dtype=torch.int32, device=X.device) if counts is None else counts
+    _need(C_out, "C_out", torch.float32)
+    _need(counts, "counts", torch.int32)
+    ws = _ws(ws, B, N, D, K, X.dtype, X.device)
+    _check(lib.kmeans_update(_ptr(X), _dt(X), _ptr(idx), _ptr(C_prev), B, N, D, K, _ptr(C_out),
+                             _ptr(counts), _ptr(ws.buf), ws.nbytes, _stream()), "kmeans_update")
+    return C_out, counts
+
+
+def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
+                 idx: Optional[torch.Tensor] = None, min_dist: Optional[torch.Tensor] = None,
+                 counts: Optional[torch.Tensor] = None, objective: bool = True,
+                 ws: Optional[Workspace] = None):
+    """Run ``iters`` Lloyd iterations, updating C in place.
+
+    Returns (C, idx, min_dist, counts, objective[B, iters] fp64 or None).
+    """
+    B, N, D, K = _shapes(X, C)
+    _need(X, "X")
+    _need(C, "C", torch.float32)
+    dev = X.device
+    idx = torch.empty((B, N), dtype=torch.int32, device=dev) if idx is None else idx
+    min_dist = torch.empty((B, N), dtype=torch.float32, device=dev) if min_dist is None else min_dist
+    counts = torch.empty((B, K), dtype=torch.int32, device=dev) if counts is None else counts
+    obj = torch.empty((B, iters), dtype=torch.float64, device=dev) if objective else None
+    for t, name, dt in ((idx, "idx", torch.int32), (min_dist, "min_dist", torch.float32),
+                        (counts, "counts", torch.int32)):
+        _need(t, name, dt)
+    ws = _ws(ws, B, N, D, K, X.dtype, dev)
+    _check(lib.kmeans_lloyd(_ptr(X), _dt(X), _ptr(C), B, N, D, K, int(iters), _ptr(idx),
+                            _ptr(min_dist), _ptr(counts), _ptr(obj), _ptr(ws.buf), ws.nbytes,
+                            _stream()), "kmeans_lloyd")
+    return C, idx, min_dist, counts, obj

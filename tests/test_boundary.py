@@ -1,0 +1,136 @@
+"""The C-ABI boundary without a GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashkmeans.h")
+LIB = os.path.join(ROOT, "paper_2608_12629_amd", "libflashkmeans.so")
+
+OK, EINVAL, EUNSUP, EWS, EHIP = 0, -1, -2, -3, -4
+F32, BF16, F16 = 0, 1, 2
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kmeans_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail(f"{LIB} not built (run __graft_entry__.build())")
+    L = ctypes.CDLL(LIB)
+    i64, i32, vp, sz = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
+    L.kmeans_workspace_bytes.argtypes = [i64, i64, i64, i64, i32]
+    L.kmeans_workspace_bytes.restype = sz
+    L.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
+    L.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
+    L.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.kmeans_status_string.argtypes = [ctypes.c_int]
+    L.kmeans_status_string.restype = ctypes.c_char_p
+    return L
+
+
+def test_header_declares_the_four_calls():
+    assert declared_functions() == ["kmeans_assign", "kmeans_lloyd", "kmeans_status_string",
+                                    "kmeans_update", "kmeans_workspace_bytes"]
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for st in (OK, EINVAL, EUNSUP, EWS, EHIP):
+        s = lib.kmeans_status_string(st).decode()
+        assert s and s != "unknown status"
+    assert lib.kmeans_status_string(12345).decode() == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    ws = lambda B, N, D, K, dt=BF16: lib.kmeans_workspace_bytes(B, N, D, K, dt)
+    assert ws(1, 8_388_608, 128, 4096) > 0
+    assert ws(1, 1000, 64, 10, F32) > 0
+    prev = 0
+    for N in (1, 100, 4096, 4097, 65536, 1 << 20):
+        cur = ws(1, N, 128, 1024)
+        assert cur >= prev
+        prev = cur
+    prev = 0
+    for K in (1, 7, 64, 1000, 4096, 32768):
+        cur = ws(1, 65536, 64, K)
+        assert cur >= prev
+        prev = cur
+    assert ws(4, 1000, 64, 10) >= ws(1, 1000, 64, 10)
+    # rejected shapes report 0
+    assert ws(0, 10, 64, 4) == 0 and ws(1, 0, 64, 4) == 0 and ws(1, 10, 64, 0) == 0
+    assert ws(1, 10, 48, 4) == 0            # D not a multiple of 32
+    assert ws(1, 10, 64, 40000) == 0        # K above the counting-sort limit
+    assert ws(1, 10, 64, 4, 7) == 0         # unknown dtype
+
+
+FAKE = 0x10000          # a non-null, 16-byte-aligned address that is never dereferenced
+
+
+def _assign(lib, X=FAKE, dt=BF16, C=FAKE, B=1, N=100, D=64, K=4, idx=FAKE, md=FAKE,
+            ws=FAKE, wsb=1 << 40):
+    return lib.kmeans_assign(X, dt, C, B, N, D, K, idx, md, ws, wsb, None)
+
+
+def _update(lib, X=FAKE, dt=BF16, idx=FAKE, Cp=FAKE, B=1, N=100, D=64, K=4, Co=FAKE, n=FAKE,
+            ws=FAKE, wsb=1 << 40):
+    return lib.kmeans_update(X, dt, idx, Cp, B, N, D, K, Co, n, ws, wsb, None)
+
+
+def _lloyd(lib, X=FAKE, dt=BF16, C=FAKE, B=1, N=100, D=64, K=4, iters=3, idx=FAKE, md=FAKE,
+           n=FAKE, obj=None, ws=FAKE, wsb=1 << 40):
+    return lib.kmeans_lloyd(X, dt, C, B, N, D, K, iters, idx, md, n, obj, ws, wsb, None)
+
+
+@pytest.mark.parametrize("call", [_assign, _update, _lloyd])
+def test_rejections_before_any_device_call(lib, call):
+    assert call(lib, X=None) == EINVAL
+    assert call(lib, X=FAKE + 4) == EINVAL          # misaligned
+    assert call(lib, dt=3) == EINVAL
+    assert call(lib, B=0) == EINVAL
+    assert call(lib, N=0) == EINVAL
+    assert call(lib, N=-5) == EINVAL
+    assert call(lib, K=0) == EINVAL
+    assert call(lib, D=0) == EINVAL
+    assert call(lib, D=48) == EUNSUP
+    assert call(lib, D=4096) == EUNSUP
+    assert call(lib, K=40000) == EUNSUP
+    assert call(lib, N=1 << 31) == EUNSUP
+    assert call(lib, ws=None) == EWS
+    assert call(lib, wsb=16) == EWS
+
+
+def test_specific_rejections(lib):
+    assert _assign(lib, C=None) == EINVAL
+    assert _assign(lib, idx=None) == EINVAL
+    assert _assign(lib, md=None) == EINVAL
+    assert _update(lib, idx=None) == EINVAL
+    assert _update(lib, Cp=None) == EINVAL
+    assert _update(lib, Co=None) == EINVAL
+    assert _update(lib, n=None) == EINVAL
+    assert _lloyd(lib, iters=0) == EINVAL
+    assert _lloyd(lib, n=None) == EINVAL
+    assert _lloyd(lib, obj=FAKE + 8) == EINVAL
+    exact = lib.kmeans_workspace_bytes(1, 100, 64, 4, BF16)
+    assert _assign(lib, wsb=exact - 1) == EWS
+
+
+def test_binding_refuses_without_library(tmp_path, monkeypatch):
+    """The Python binding raises instead of falling back when the library is absent."""
+    import importlib
+    import paper_2608_12629_amd.kmeans as km
+    monkeypatch.setattr(km, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        km._load()
+    importlib.reload(km)  # restore the module state with the real library

@@ -1,0 +1,222 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Teacher-forced steps (the oracle consumes the GPU's own C_t for the assignment
+and the GPU's own idx_t for the update) on the same seeded inputs, at sizes the
+oracle finishes in seconds; the full-size workloads are checked on sampled rows
+for the assignment and in full for the update.  Also: edge cases, determinism,
+and that kmeans_lloyd equals the composition of its two steps.
+"""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from parity import check_assign, check_update, raw, tol_for
+from paper_2608_12629_amd.synth import make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def km():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2608_12629_amd import kmeans
+    return kmeans
+
+
+def teacher_forced(km, o, X, C0, dtype, iters, rows=None):
+    """Run `iters` assign/update steps on the GPU and check each against the oracle."""
+    Xd = X.cuda()
+    C = C0.cuda().clone()
+    Xr = raw(X)
+    Xs = np.ascontiguousarray(Xr[:, rows]) if rows is not None else Xr
+    reports = []
+    ws = km.Workspace(X.shape[0], X.shape[1], X.shape[2], C.shape[1], X.dtype)
+    for t in range(iters):
+        idx, md = km.kmeans_assign(Xd, C, ws=ws)
+        C1, n = km.kmeans_update(Xd, idx, C, ws=ws)
+        torch.cuda.synchronize()
+        C64 = C.cpu().double().numpy()
+        ig, mg = idx.cpu().numpy(), md.cpu().numpy()
+        if rows is not None:
+            ig_s, mg_s = ig[:, rows], mg[:, rows]
+        else:
+            ig_s, mg_s = ig, mg
+        rep = check_assign(o, Xs, dtype, C64, ig_s, mg_s) if rows is None else \
+            check_assign_rows(o, Xs, dtype, C64, ig_s, mg_s)
+        err = check_update(o, Xr, dtype, ig, C64, C1.cpu().numpy(), n.cpu().numpy())
+        say(f"  t={t} mismatches={rep.mismatches} (exempt pts {rep.exempt_points}) "
+            f"md_err={rep.worst_md_err:.2e} J={rep.J_gpu:.6e}/{rep.J_oracle:.6e} C_err={err:.2e}")
+        reports.append(rep)
+        C = C1
+    return reports
+
+
+def check_assign_rows(o, Xs, dtype, C64, ig, mg):
+    return check_assign(o, Xs, dtype, C64, ig, mg)
+
+
+# ----------------------------------------------------------------- workloads
+SMALL = {
+    "cfg1_full": dict(cfg=1),
+    "cfg2_small": dict(cfg=2, N=65536, K=256),
+    "cfg3_small": dict(cfg=3, N=65536, K=512),
+    "cfg4_small": dict(cfg=4, B=8, N=4096),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_teacher_forced_small(km, oracle, name):
+    kw = dict(SMALL[name])
+    w = make_workload(kw.pop("cfg"), **kw)
+    say(f"[{name}] {w.name} B={w.B} N={w.N} D={w.D} K={w.K} {w.dtype}")
+    teacher_forced(km, oracle, w.X, w.C0, w.dtype, min(w.iters, 4))
+
+
+def test_cfg4_full_teacher_forced(km, oracle):
+    w = make_workload(4)
+    say(f"[cfg4] {w.name}")
+    teacher_forced(km, oracle, w.X, w.C0, w.dtype, 3)
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_full_size_sampled(km, oracle, cfg):
+    """Full-size workload: assignment checked on 4096 sampled rows, update in full."""
+    w = make_workload(cfg)
+    rows = np.sort(np.random.default_rng(cfg).choice(w.N, 4096, replace=False))
+    say(f"[cfg{cfg} full] {w.name}")
+    teacher_forced(km, oracle, w.X, w.C0, w.dtype, 2, rows=rows)
+
+
+# --------------------------------------------------------------- edge cases
+def _blobs(B, N, D, K, dtype, seed, spread=1.0):
+    g = torch.Generator().manual_seed(seed)
+    centres = torch.rand((B, K, D), generator=g) * 2 - 1
+    lab = torch.randint(0, K, (B, N), generator=g)
+    X = torch.gather(centres, 1, lab[..., None].expand(B, N, D)) + spread * 0.1 * torch.randn(
+        (B, N, D), generator=g)
+    X = X.to(dtype)
+    C0 = X[:, :K].float().clone()
+    return X, C0
+
+
+DT = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+SHAPES = [
+    # (B, N, D, K, dtype)
+    (1, 1, 64, 1, "bf16"),            # single point, single centroid
+    (1, 1000, 64, 1, "f16"),          # K = 1
+    (1, 777, 128, 100, "bf16"),       # ragged N and K
+    (1, 5000, 32, 7, "f32"),          # fp32 D = 32
+    (1, 4097, 64, 300, "f32"),        # ragged sort chunk
+    (1, 2049, 128, 64, "f32"),        # fp32 D = 128
+    (1, 3000, 256, 50, "bf16"),       # D = 256
+    (1, 3000, 256, 33, "f16"),
+    (1, 3000, 32, 65, "bf16"),        # D = 32
+    (3, 2500, 64, 40, "f16"),         # batched, ragged
+    (1, 300, 64, 300, "bf16"),        # K = N
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_edge_shapes(km, oracle, shape):
+    B, N, D, K, dt = shape
+    X, C0 = _blobs(B, N, D, K, DT[dt], seed=N * 7 + K)
+    say(f"[edge] B={B} N={N} D={D} K={K} {dt}")
+    teacher_forced(km, oracle, X, C0, dt, 2)
+
+
+def test_duplicates_and_empty_clusters(km, oracle):
+    """Duplicate centroids (lower index wins), duplicate points, an empty far cluster."""
+    X, C0 = _blobs(1, 3000, 64, 16, torch.bfloat16, seed=5)
+    X[0, 100:200] = X[0, 50]                 # 101 identical points
+    C0[0, 9] = C0[0, 3]                      # duplicate centroid: 9 must never win
+    C0[0, 12] = 1e3                          # far away: empty cluster
+    Xd, C = X.cuda(), C0.cuda()
+    idx, md = km.kmeans_assign(Xd, C)
+    C1, n = km.kmeans_update(Xd, idx, C)
+    torch.cuda.synchronize()
+    ig = idx.cpu().numpy()
+    assert not (ig == 9).any() and not (ig == 12).any()
+    assert n[0, 9].item() == 0 and n[0, 12].item() == 0
+    assert torch.equal(C1[0, 12].cpu(), C0[0, 12]) and torch.equal(C1[0, 9].cpu(), C0[0, 9])
+    assert len(set(ig[0, 100:200].tolist() + [ig[0, 50]])) == 1
+    teacher_forced(km, oracle, X, C0, "bf16", 2)
+
+
+def test_all_points_one_cluster(km, oracle):
+    """Maximal skew: every point in one cluster (one sorted run spans every chunk)."""
+    g = torch.Generator().manual_seed(3)
+    X = (0.05 * torch.randn((1, 20000, 128), generator=g)).to(torch.bfloat16)
+    C0 = torch.zeros((1, 4, 128))
+    C0[0, 1:] = 50.0
+    Xd = X.cuda()
+    idx, md = km.kmeans_assign(Xd, C0.cuda())
+    C1, n = km.kmeans_update(Xd, idx, C0.cuda())
+    torch.cuda.synchronize()
+    assert n[0].tolist() == [20000, 0, 0, 0]
+    mean = X[0].double().mean(0)
+    rel = (C1[0, 0].cpu().double() - mean).norm() / mean.norm()
+    assert rel < 1e-3
+    teacher_forced(km, oracle, X, C0, "bf16", 1)
+
+
+def test_points_as_centroids(km):
+    """C = X: every point is its own nearest centroid at distance 0."""
+    g = torch.Generator().manual_seed(11)
+    X = torch.randn((1, 256, 64), generator=g).to(torch.bfloat16)
+    idx, md = km.kmeans_assign(X.cuda(), X.float().cuda())
+    torch.cuda.synchronize()
+    assert idx.cpu()[0].tolist() == list(range(256))
+    assert md.abs().max().item() <= 1e-3 * float((X.float() ** 2).sum(-1).max())
+
+
+# ------------------------------------------------------- composition, determinism
+@pytest.mark.parametrize("cfg,kw", [(1, {}), (3, dict(N=65536, K=512)), (4, dict(B=8, N=4096))])
+def test_lloyd_equals_steps_and_is_deterministic(km, oracle, cfg, kw):
+    w = make_workload(cfg, **kw)
+    Xd = w.X.cuda()
+    iters = 3
+    C_a, idx_a, md_a, n_a, obj_a = km.kmeans_lloyd(Xd, w.C0.cuda().clone(), iters)
+    C_b, idx_b, md_b, n_b, obj_b = km.kmeans_lloyd(Xd, w.C0.cuda().clone(), iters)
+    torch.cuda.synchronize()
+    for a, b in ((C_a, C_b), (idx_a, idx_b), (md_a, md_b), (n_a, n_b), (obj_a, obj_b)):
+        assert torch.equal(a, b), "two identical runs differ"
+    C = w.C0.cuda().clone()
+    objs = []
+    for t in range(iters):
+        idx, md = km.kmeans_assign(Xd, C)
+        objs.append(md.double().sum(-1))
+        C, n = km.kmeans_update(Xd, idx, C)
+    torch.cuda.synchronize()
+    assert torch.equal(C, C_a) and torch.equal(idx, idx_a) and torch.equal(md, md_a)
+    assert torch.equal(n, n_a)
+    J = torch.stack(objs, -1)
+    assert torch.allclose(J, obj_a, rtol=1e-12, atol=0)
+    # the objective never increases (up to the contract's relative tolerance)
+    o = obj_a.cpu().numpy()
+    assert np.all(np.diff(o, axis=-1) <= tol_for(w.dtype) * o[:, :-1])
+
+
+def test_mass_conservation_full_cfg3(km):
+    """sum_k n_k c'_k = sum_i x_i at the full 8M-point workload (no oracle needed)."""
+    w = make_workload(3)
+    Xd = w.X.cuda()
+    idx, md = km.kmeans_assign(Xd, w.C0.cuda())
+    C1, n = km.kmeans_update(Xd, idx, w.C0.cuda())
+    torch.cuda.synchronize()
+    assert int(n.sum()) == w.N
+    lhs = (n.double()[0, :, None] * C1.double()[0]).sum(0)
+    rhs = Xd.double()[0].sum(0)
+    scale = Xd.double()[0].abs().sum(0)
+    assert ((lhs - rhs).abs() <= 1e-5 * scale).all()
+    assert (md >= 0).all() and int(idx.min()) >= 0 and int(idx.max()) < w.K
