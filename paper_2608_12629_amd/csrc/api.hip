@@ -14,7 +14,8 @@ static size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
   Workspace w{};
-  w.n_assign_blocks = (N + assign_points_per_block(dt, (int)D) - 1) / assign_points_per_block(dt, (int)D);
+  const int64_t ppb = assign_points_per_block(dt, D);
+  w.n_assign_blocks = (N + ppb - 1) / ppb;
   w.n_sort_chunks = (N + SORT_WC - 1) / SORT_WC;
   w.n_seg = (w.n_sort_chunks + SORT_SEG - 1) / SORT_SEG;
   w.n_red_chunks = (N + RED_CR - 1) / RED_CR;
@@ -25,8 +26,9 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
     o = align_up(o + bytes);
     return r;
   };
-  w.chat = take((size_t)(B * K * D) * dt_bytes(dt));
-  w.cinit = (float*)take((size_t)(B * K) * 4);
+  w.Kp = kpad(K);
+  w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
+  w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
   w.objpart = (double*)take((size_t)(B * w.n_assign_blocks) * 8);
   w.hist = (int32_t*)take((size_t)(B * w.n_sort_chunks * K) * 4);
   w.segsum = (int32_t*)take((size_t)(B * w.n_seg * K) * 4);
@@ -103,7 +105,7 @@ int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t 
   if ((rc = check_device())) return rc;
   hipStream_t s = (hipStream_t)stream;
   const Workspace w = carve(ws, B, N, D, K, xdtype);
-  if ((rc = hip_status(launch_prep(C, xdtype, B * K, D, w.chat, w.cinit, s)))) return rc;
+  if ((rc = hip_status(launch_prep(C, xdtype, B, K, w.Kp, D, w.chat, w.cinit, s)))) return rc;
   return hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s));
 }
 
@@ -133,7 +135,7 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   hipStream_t s = (hipStream_t)stream;
   const Workspace w = carve(ws, B, N, D, K, xdtype);
   for (int t = 0; t < iters; ++t) {
-    if ((rc = hip_status(launch_prep(C, xdtype, B * K, D, w.chat, w.cinit, s)))) return rc;
+    if ((rc = hip_status(launch_prep(C, xdtype, B, K, w.Kp, D, w.chat, w.cinit, s)))) return rc;
     if ((rc = hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s)))) return rc;
     if (objective && (rc = hip_status(launch_objective(w, B, iters, t, objective, s)))) return rc;
     if ((rc = hip_status(launch_update(X, xdtype, idx, C, w, B, N, D, K, C, counts, s))))

@@ -84,30 +84,47 @@ __device__ inline f32x4 mfma_chunk(const uint4& a, const uint4& b, f32x4 acc) {
   }
 }
 
+
+// acc += A-chunk x B-chunk on a 32x32x16 tile (16-bit storage types).
+template <int DT>
+__device__ inline f32x16 mfma32_chunk(const uint4& a, const uint4& b, f32x16 acc) {
+  if constexpr (DT == DT_BF16) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // prep: c^ = round(c) to the storage type and cinit = -|c^|^2 / 2 (fp32),
 // one wave per centroid row; the squared norm is summed lane-strided and then
 // by a fixed xor butterfly, so every lane (and every call) gets the same bits.
+// Rows K..Kp-1 of each instance are padding: zero, with cinit = -FLT_MAX.
 template <int DT>
-__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, int64_t rows,
-                                                   int D, void* __restrict__ chat,
+__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, int64_t B, int K,
+                                                   int Kp, int D, void* __restrict__ chat,
                                                    float* __restrict__ cinit) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const float* c = C + row * D;
+  if (row >= B * Kp) return;
+  const int64_t b = row / Kp;
+  const int k = (int)(row % Kp);
+  const bool pad = k >= K;
+  const float* c = C + (b * K + (pad ? 0 : k)) * D;
   float ss = 0.f;
   if constexpr (DT == DT_F32) {
     float* out = (float*)chat + row * D;
     for (int d = lane; d < D; d += 64) {
-      const float v = c[d];
+      const float v = pad ? 0.f : c[d];
       out[d] = v;
       ss = __builtin_fmaf(v, v, ss);
     }
   } else {
     uint16_t* out = (uint16_t*)chat + row * D;
     for (int d = lane; d < D; d += 64) {
-      const uint16_t h = Elem<DT>::narrow(c[d]);
+      const uint16_t h = pad ? (uint16_t)0 : Elem<DT>::narrow(c[d]);
       out[d] = h;
       const float v = Elem<DT>::widen(h);
       ss = __builtin_fmaf(v, v, ss);
@@ -115,7 +132,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, 
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
-  if (lane == 0) cinit[row] = -0.5f * ss;
+  if (lane == 0) cinit[row] = pad ? -0x1.fffffep127f : -0.5f * ss;
 }
 
 // ---------------------------------------------------------------------------
@@ -125,7 +142,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, 
 template <int DT, int CPL, int NSUB>
 __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
-    int N, int K, int32_t* __restrict__ idx, float* __restrict__ min_dist,
+    int N, int K, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
     double* __restrict__ objpart) {
   constexpr int RC = 4 * CPL;              // 16-byte chunks per row
   constexpr int SWZ = RC < 16 ? RC - 1 : 15;
@@ -144,8 +161,8 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
   const int lane = tid & 63, wave = tid >> 6;
   const int m = lane & 15, g = lane >> 4;
   X += (size_t)b * N * RC;
-  chat += (size_t)b * K * RC;
-  cinit += (size_t)b * K;
+  chat += (size_t)b * Kp * RC;
+  cinit += (size_t)b * Kp;
   idx += (size_t)b * N;
   min_dist += (size_t)b * N;
 
@@ -261,6 +278,296 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
 }
 
+// ---------------------------------------------------------------------------
+// Resident-X assignment on 32x32x16 bf16/fp16 MFMA tiles, software-pipelined.
+//
+// Tile layout: 32 centroids (A rows) x 32 points (B columns) per instruction.
+// Lane l = 32 h + n supplies point column n and centroid row n for the
+// k-slice h (each lane group holds one contiguous half of the D dimensions)
+// and receives accumulator rows 8 q + 4 h + r (q, r = 0..3) of column n.
+// Each wave keeps NSUB 32-point column tiles in registers for the whole
+// kernel; centroids stream through LDS in stages of TCS = 2 tiles.
+//
+// Pipelining.  On this GPU the matrix pipe and the vector ALU overlap only
+// within one wave's instruction stream (a wave that only issues vector
+// instructions does not run beside another wave's MFMAs).  So the MFMAs of
+// tile t and the epilogue of tile t-1 are written into the same basic block,
+// on two accumulator sets, for the scheduler to interleave; NSUB independent
+// accumulation chains keep the matrix pipe fed.
+//
+// Epilogue.  The accumulator starts at -|c^|^2/2 - Q, with Q a bound on
+// |x|^2/2 over the workgroup's points plus a margin, so every score
+// s' = <x, c^> - |c^|^2/2 - Q is strictly negative and orders the centroids
+// like the distance does.  The lane's position j = 4 q + r is written into the
+// 4 low mantissa bits of each score (one and-or), a max3 tree picks the
+// tile's best (for negative floats larger low bits mean more negative, so on
+// equal upper bits the lowest position wins), and a strict compare on the
+// masked value keeps the earliest tile.  Scores within 16 ulp of each other
+// therefore count as ties and go to the lowest index; nothing else changes.
+// Padding rows score -FLT_MAX (an infinity with position bits would be a
+// signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
+template <int CPL, int LOADS>
+struct PipeStage {
+  u32x4 v[LOADS];  // native vectors: the struct stays in registers
+  float n;
+};
+
+// Per-lane LDS byte offsets, fixed for the whole kernel: where this thread
+// stores its stage chunks, and where it reads its A chunks and scores.
+template <int CPL, int LOADS>
+struct PipeOffsets {
+  int store[LOADS];  // swizzled slot of chunk tid + u * 256 of a stage
+  int a[CPL];        // chunk h * CPL + c of centroid row n of tile 0
+  int n_store;       // score slot written by this thread
+  int n_read;        // first score read by this lane (rows 4 h .. 4 h + 3)
+};
+
+// Stage = two 32-centroid tiles: TCS rows of RC chunks, then TCS scores.
+template <int CPL>
+struct PipeLayout {
+  static constexpr int TCS = ASSIGN_TCS, RC = 2 * CPL;
+  static constexpr int SWZ = RC < 16 ? RC - 1 : 15;
+  static constexpr int CHUNKS = TCS * RC * 16;          // bytes of centroid chunks
+  static constexpr int STAGE = CHUNKS + TCS * 4;         // bytes per stage buffer
+  static constexpr int TILE = 32 * RC * 16;              // bytes per tile of chunks
+};
+
+template <int CPL, int LOADS>
+__device__ __forceinline__ void pipe_offsets(PipeOffsets<CPL, LOADS>& o, int tid, int n, int h) {
+  using L = PipeLayout<CPL>;
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) {
+    const int q = tid + u * ASSIGN_THREADS;
+    const int r = q / L::RC, c = q % L::RC;
+    o.store[u] = (r * L::RC + (c ^ (r & L::SWZ))) * 16;
+  }
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) o.a[c] = (n * L::RC + ((h * CPL + c) ^ (n & L::SWZ))) * 16;
+  o.n_store = L::CHUNKS + (tid & (L::TCS - 1)) * 4;
+  o.n_read = L::CHUNKS + 16 * h;
+}
+
+template <int CPL, int LOADS>
+__device__ __forceinline__ void pipe_load_stage(PipeStage<CPL, LOADS>& g, const u32x4* __restrict__ chat,
+                                                const float* __restrict__ cinit, int st, int tid) {
+  using L = PipeLayout<CPL>;
+  const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) g.v[u] = src[tid + u * ASSIGN_THREADS];
+  g.n = cinit[st * L::TCS + (tid & (L::TCS - 1))];
+}
+
+// LDS accesses at a per-lane offset plus a compile-time byte offset.
+template <typename T>
+__device__ __forceinline__ T& lds_at(char* base, int lane_off, int imm) {
+  return *reinterpret_cast<T*>(base + lane_off + imm);
+}
+
+template <int BUF, int CPL, int LOADS>
+__device__ __forceinline__ void pipe_store_stage(const PipeStage<CPL, LOADS>& g, char* lds,
+                                                 const PipeOffsets<CPL, LOADS>& o, float Q) {
+  using L = PipeLayout<CPL>;
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) lds_at<u32x4>(lds, o.store[u], BUF * L::STAGE) = g.v[u];
+  lds_at<float>(lds, o.n_store, BUF * L::STAGE) = g.n - Q;
+}
+
+// The MFMAs of one 32-centroid tile into acc; each chain starts from the scores' init.
+template <int DT, int BUF, int TILE, int CPL, int NSUB, int LOADS>
+__device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 (&xr)[NSUB][CPL],
+                                               char* lds, const PipeOffsets<CPL, LOADS>& o) {
+  using L = PipeLayout<CPL>;
+  f32x16 cin;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 v = lds_at<f32x4>(lds, o.n_read, BUF * L::STAGE + (TILE * 32 + 8 * q) * 4);
+    cin[4 * q + 0] = v[0];
+    cin[4 * q + 1] = v[1];
+    cin[4 * q + 2] = v[2];
+    cin[4 * q + 3] = v[3];
+  }
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const uint4 a = lds_at<uint4>(lds, o.a[c], BUF * L::STAGE + TILE * L::TILE);
+#pragma unroll
+    for (int p = 0; p < NSUB; ++p) acc[p] = mfma32_chunk<DT>(a, xr[p][c], c == 0 ? cin : acc[p]);
+  }
+}
+
+// Packed-key arg-max of one tile into the running (best, code) of each column tile.
+template <int NSUB>
+__device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_t tcode,
+                                              float (&best)[NSUB], uint32_t (&code)[NSUB]) {
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    float k[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      k[j] = __uint_as_float((__float_as_uint(acc[p][j]) & ~15u) | (uint32_t)j);
+    const float t0 = __builtin_fmaxf(__builtin_fmaxf(k[0], k[1]), k[2]);
+    const float t1 = __builtin_fmaxf(__builtin_fmaxf(k[3], k[4]), k[5]);
+    const float t2 = __builtin_fmaxf(__builtin_fmaxf(k[6], k[7]), k[8]);
+    const float t3 = __builtin_fmaxf(__builtin_fmaxf(k[9], k[10]), k[11]);
+    const float t4 = __builtin_fmaxf(__builtin_fmaxf(k[12], k[13]), k[14]);
+    const float u0 = __builtin_fmaxf(__builtin_fmaxf(t0, t1), t2);
+    const float u1 = __builtin_fmaxf(__builtin_fmaxf(t3, t4), k[15]);
+    const uint32_t mb = __float_as_uint(__builtin_fmaxf(u0, u1));
+    const float mm = __uint_as_float(mb & ~15u);
+    const bool gt = mm > best[p];
+    best[p] = gt ? mm : best[p];
+    code[p] = gt ? ((mb & 15u) | tcode) : code[p];
+  }
+}
+
+// One stage in buffer BUF: prefetch stage `next` from HBM/L2, run tile 0 on
+// accB beside the epilogue of the previous tile (accA), tile 1 on accA beside
+// the epilogue of tile 0, then store the prefetch into the other buffer.
+template <int DT, int BUF, int CPL, int NSUB, int LOADS>
+__device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
+                                           const uint4 (&xr)[NSUB][CPL], char* lds,
+                                           const PipeOffsets<CPL, LOADS>& o, const u32x4* chat,
+                                           const float* cinit, float Q, int tid,
+                                           uint32_t& prev_code, float (&best)[NSUB],
+                                           uint32_t (&code)[NSUB]) {
+  PipeStage<CPL, LOADS> pre;
+  pipe_load_stage<CPL, LOADS>(pre, chat, cinit, next, tid);
+  // issue the prefetch first: left to the scheduler it drifts into the middle
+  // of the stage and the store at the end waits for it
+  __builtin_amdgcn_sched_barrier(0);
+  const uint32_t code0 = (uint32_t)(2 * st) << 4, code1 = (uint32_t)(2 * st + 1) << 4;
+  pipe_mfma_tile<DT, BUF, 0, CPL, NSUB, LOADS>(accB, xr, lds, o);
+  pipe_epilogue<NSUB>(accA, prev_code, best, code);
+  pipe_mfma_tile<DT, BUF, 1, CPL, NSUB, LOADS>(accA, xr, lds, o);
+  pipe_epilogue<NSUB>(accB, code0, best, code);
+  prev_code = code1;
+  pipe_store_stage<BUF ^ 1, CPL, LOADS>(pre, lds, o, Q);
+  // interleave: one MFMA, then a few vector instructions, repeated
+#pragma unroll
+  for (int i = 0; i < 2 * NSUB * CPL; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+  }
+  __syncthreads();
+}
+
+template <int DT, int CPL, int NSUB>
+__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
+    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
+    int N, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
+    double* __restrict__ objpart) {
+  static_assert(DT != DT_F32, "16-bit storage types only");
+  using L = PipeLayout<CPL>;
+  static_assert(L::TCS == 64 && ASSIGN_KPAD % L::TCS == 0, "stage = two tiles, K padded to stages");
+  constexpr int RC = L::RC;
+  constexpr int PPW = 32 * NSUB;           // points per wave
+  constexpr int PPB = 4 * PPW;             // points per workgroup
+  constexpr int LOADS = L::TCS * RC / ASSIGN_THREADS;
+  static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * RC, "stage must split evenly");
+
+  __shared__ __attribute__((aligned(16))) char lds[2 * L::STAGE];
+  __shared__ float lds_q[4];
+  __shared__ double lds_obj[4];
+
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  X += (size_t)b * N * RC;
+  const u32x4* chat4 = reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * RC;
+  cinit += (size_t)b * Kp;
+  idx += (size_t)b * N;
+  min_dist += (size_t)b * N;
+  const int nst = Kp / L::TCS;
+
+  PipeOffsets<CPL, LOADS> o;
+  pipe_offsets<CPL, LOADS>(o, tid, n, h);
+  PipeStage<CPL, LOADS> pre;
+  pipe_load_stage<CPL, LOADS>(pre, chat4, cinit, 0, tid);
+
+  const int pbase = blockIdx.x * PPB + wave * PPW;
+  uint4 xr[NSUB][CPL];
+  float xn[NSUB];
+  float xmax = 0.f;
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    const int pt = pbase + p * 32 + n;
+    const bool ok = pt < N;
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      xr[p][c] = ok ? X[(size_t)pt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
+      ss = chunk_sumsq<DT>(xr[p][c], ss);
+    }
+    ss += __shfl_xor(ss, 32);
+    xn[p] = ss;
+    xmax = __builtin_fmaxf(xmax, ss);
+  }
+#pragma unroll
+  for (int msk = 1; msk < 64; msk <<= 1) xmax = __builtin_fmaxf(xmax, __shfl_xor(xmax, msk));
+  if (lane == 0) lds_q[wave] = xmax;
+  __syncthreads();
+  // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding)
+  const float Q = __builtin_fmaf(
+      0.5f * __builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])),
+      1.0f + 0x1p-8f, 1e-30f);
+
+  float best[NSUB];
+  uint32_t code[NSUB];
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    best[p] = -__builtin_inff();
+    code[p] = 0;
+  }
+  // accA holds the previous tile; before the first tile it is a dummy at the
+  // most negative score, which every real score replaces
+  f32x16 accA[NSUB], accB[NSUB];
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) accA[p][j] = -0x1.fffffep127f;
+  uint32_t prev_code = 0;
+
+  pipe_store_stage<0, CPL, LOADS>(pre, lds, o, Q);
+  __syncthreads();
+  int st = 0;
+  for (; st + 2 <= nst; st += 2) {   // two stages per trip: buffer offsets are constants
+    pipe_stage<DT, 0, CPL, NSUB, LOADS>(st, st + 1, accA, accB, xr, lds, o, chat4, cinit, Q, tid,
+                                        prev_code, best, code);
+    pipe_stage<DT, 1, CPL, NSUB, LOADS>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr,
+                                        lds, o, chat4, cinit, Q, tid, prev_code, best, code);
+  }
+  if (st < nst)
+    pipe_stage<DT, 0, CPL, NSUB, LOADS>(st, st, accA, accB, xr, lds, o, chat4, cinit, Q, tid,
+                                        prev_code, best, code);
+  pipe_epilogue<NSUB>(accA, prev_code, best, code);
+
+  double obj = 0.0;
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) {
+    float v = best[p];
+    const uint32_t j = code[p] & 15u;
+    int i = (int)((code[p] >> 4) * 32 + 8 * (j >> 2) + 4 * h + (j & 3));
+    const float vo = __shfl_xor(v, 32);
+    const int io = __shfl_xor(i, 32);
+    const bool take = (vo > v) || (vo == v && io < i);
+    v = take ? vo : v;
+    i = take ? io : i;
+    const int pt = pbase + p * 32 + n;
+    if (h == 0 && pt < N) {
+      const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Q, xn[p]), 0.f);
+      idx[pt] = i;
+      min_dist[pt] = md;
+      obj += (double)md;
+    }
+  }
+#pragma unroll
+  for (int msk = 1; msk < 64; msk <<= 1) obj += __shfl_xor(obj, msk);
+  if (lane == 0) lds_obj[wave] = obj;
+  __syncthreads();
+  if (tid == 0)
+    objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
+}
+
 // Sum of one instance's workgroup partials in a fixed order, in fp64.
 __global__ __launch_bounds__(256) void objective_kernel(const double* __restrict__ part, int nblk,
                                                         int iters, int t, double* __restrict__ out) {
@@ -278,12 +585,15 @@ __global__ __launch_bounds__(256) void objective_kernel(const double* __restrict
 }
 
 // ---------------------------------------------------------------------------
-hipError_t launch_prep(const float* C, int dt, int64_t rows, int64_t D, void* chat, float* cinit,
-                       hipStream_t s) {
-  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-  if (dt == DT_BF16) prep_kernel<DT_BF16><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
-  else if (dt == DT_F16) prep_kernel<DT_F16><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
-  else prep_kernel<DT_F32><<<grid, block, 0, s>>>(C, rows, (int)D, chat, cinit);
+hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp, int64_t D,
+                       void* chat, float* cinit, hipStream_t s) {
+  const dim3 grid((unsigned)((B * Kp + 3) / 4)), block(256);
+  if (dt == DT_BF16)
+    prep_kernel<DT_BF16><<<grid, block, 0, s>>>(C, B, (int)K, (int)Kp, (int)D, chat, cinit);
+  else if (dt == DT_F16)
+    prep_kernel<DT_F16><<<grid, block, 0, s>>>(C, B, (int)K, (int)Kp, (int)D, chat, cinit);
+  else
+    prep_kernel<DT_F32><<<grid, block, 0, s>>>(C, B, (int)K, (int)Kp, (int)D, chat, cinit);
   return hipGetLastError();
 }
 
@@ -293,7 +603,8 @@ static hipError_t launch_resident(const void* X, const Workspace& w, int64_t B, 
   constexpr int NSUB = CPL <= 4 ? 8 : 4;
   const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
   assign_resident_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
-      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)K, idx, min_dist, w.objpart);
+      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)K, (int)w.Kp, idx, min_dist,
+      w.objpart);
   return hipGetLastError();
 }
 
@@ -310,11 +621,33 @@ static hipError_t launch_resident_dt(const void* X, const Workspace& w, int64_t 
   }
 }
 
+template <int DT, int CPL, int NSUB>
+static hipError_t launch_pipe(const void* X, const Workspace& w, int64_t B, int64_t N,
+                              int32_t* idx, float* min_dist, hipStream_t s) {
+  const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
+  assign_pipe_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
+      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)w.Kp, idx, min_dist, w.objpart);
+  return hipGetLastError();
+}
+
+// NSUB must agree with assign_nsub16(D).
+template <int DT>
+static hipError_t launch_pipe_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
+                                 int64_t D, int32_t* idx, float* min_dist, hipStream_t s) {
+  switch (D) {
+    case 32: return launch_pipe<DT, 2, 4>(X, w, B, N, idx, min_dist, s);
+    case 64: return launch_pipe<DT, 4, 4>(X, w, B, N, idx, min_dist, s);
+    case 128: return launch_pipe<DT, 8, 2>(X, w, B, N, idx, min_dist, s);
+    case 256: return launch_pipe<DT, 16, 1>(X, w, B, N, idx, min_dist, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
   if (!assign_resident_ok(dt, D)) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return launch_resident_dt<DT_BF16>(X, w, B, N, D, K, idx, min_dist, s);
-  if (dt == DT_F16) return launch_resident_dt<DT_F16>(X, w, B, N, D, K, idx, min_dist, s);
+  if (dt == DT_BF16) return launch_pipe_dt<DT_BF16>(X, w, B, N, D, idx, min_dist, s);
+  if (dt == DT_F16) return launch_pipe_dt<DT_F16>(X, w, B, N, D, idx, min_dist, s);
   return launch_resident_dt<DT_F32>(X, w, B, N, D, K, idx, min_dist, s);
 }
 

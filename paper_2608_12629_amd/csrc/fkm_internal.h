@@ -15,6 +15,8 @@ inline int dt_bytes(int dt) { return dt == DT_F32 ? 4 : 2; }
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ---- tuning constants -------------------------------------------------------
 // Assignment (resident-X kernel): 256 threads = 4 waves per workgroup; each
@@ -22,6 +24,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // LDS in stages of ASSIGN_TCS rows.
 constexpr int ASSIGN_THREADS = 256;
 constexpr int ASSIGN_TCS = 64;
+// The rounded centroids and their norms are stored padded to a whole number of
+// ASSIGN_KPAD-row stages: padding rows are zero with the most negative score.
+constexpr int ASSIGN_KPAD = 64;
+inline int64_t kpad(int64_t K) { return (K + ASSIGN_KPAD - 1) / ASSIGN_KPAD * ASSIGN_KPAD; }
 // Update: the counting sort works on chunks of SORT_WC points (one wave ranks
 // a chunk); chunk histograms are scanned in segments of SORT_SEG chunks; the
 // segmented sum gives each wave RED_CR consecutive entries of the sorted order.
@@ -40,11 +46,14 @@ inline bool row_bytes_ok(int dt, int64_t D) {
   return D % 32 == 0 && rb >= 64 && rb <= 8192 && (rb & (rb - 1)) == 0;
 }
 
-inline int assign_nsub(int dt, int D) {
-  const int cpl = D * dt_bytes(dt) / 64;  // 16-byte chunks per lane
-  return cpl <= 4 ? 8 : 4;
+// Points per assignment workgroup.  16-bit storage: 32x32x16 MFMA tiles, 4
+// waves x NSUB x 32 points (NSUB = 4 up to D = 64, 2 at 128, 1 at 256).  fp32: 16x16x4
+// MFMA tiles, 4 waves x NSUB x 16 points (NSUB = 8 up to 256-byte rows, else 4).
+inline int assign_nsub16(int64_t D) { return D <= 64 ? 4 : (D <= 128 ? 2 : 1); }
+inline int64_t assign_points_per_block(int dt, int64_t D) {
+  if (dt != DT_F32) return 4 * 32 * assign_nsub16(D);
+  return 4 * 16 * (D * 4 / 64 <= 4 ? 8 : 4);
 }
-inline int64_t assign_points_per_block(int dt, int D) { return 64 * assign_nsub(dt, D); }
 
 // The resident-X assignment kernel handles these row widths (bytes per point).
 inline bool assign_resident_ok(int dt, int64_t D) {
@@ -54,8 +63,8 @@ inline bool assign_resident_ok(int dt, int64_t D) {
 
 // ---- workspace layout -------------------------------------------------------
 struct Workspace {
-  void* chat;      // [B,K,D] centroids rounded to the storage type
-  float* cinit;    // [B,K]   -1/2 * squared norm of each rounded centroid
+  void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad(K))
+  float* cinit;    // [B,Kp]   -1/2 * squared norm of each rounded centroid
   double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
   int32_t* hist;   // [B,n_sort_chunks,K] chunk histograms, then chunk start offsets
   int32_t* segsum; // [B,n_seg,K] histogram sums per segment of chunks
@@ -63,15 +72,15 @@ struct Workspace {
   int32_t* perm;   // [B,N] point ids sorted by cluster
   float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by chunk ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
-  int64_t n_assign_blocks, n_sort_chunks, n_seg, n_red_chunks;
+  int64_t Kp, n_assign_blocks, n_sort_chunks, n_seg, n_red_chunks;
   size_t total;
 };
 
 Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt);
 
 // ---- launchers (return hipSuccess or the launch error) ----------------------
-hipError_t launch_prep(const float* C, int dt, int64_t rows, int64_t D, void* chat, float* cinit,
-                       hipStream_t s);
+hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp, int64_t D,
+                       void* chat, float* cinit, hipStream_t s);
 hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
