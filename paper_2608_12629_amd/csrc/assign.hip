@@ -568,16 +568,27 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
     objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
 }
 
-// Sum of one instance's workgroup partials in a fixed order, in fp64.
-__global__ __launch_bounds__(256) void objective_kernel(const double* __restrict__ part, int nblk,
-                                                        int iters, int t, double* __restrict__ out) {
-  __shared__ double s[256];
+// Sum of one instance's workgroup partials in a fixed order, in fp64: thread t
+// sums partials t, t + 1024, ... (eight loads in flight), then a tree in LDS.
+__global__ __launch_bounds__(1024) void objective_kernel(const double* __restrict__ part, int nblk,
+                                                         int iters, int t, double* __restrict__ out) {
+  __shared__ double s[1024];
   const int b = blockIdx.x;
+  const double* pb = part + (size_t)b * nblk;
   double a = 0.0;
-  for (int i = threadIdx.x; i < nblk; i += 256) a += part[(size_t)b * nblk + i];
+  for (int i0 = 0; i0 < nblk; i0 += 8 * 1024) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 1024 + (int)threadIdx.x;
+      v[u] = i < nblk ? pb[i] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a += v[u];
+  }
   s[threadIdx.x] = a;
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
+  for (int w = 512; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
     __syncthreads();
   }
@@ -653,7 +664,7 @@ hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, i
 
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
                             hipStream_t s) {
-  objective_kernel<<<dim3((unsigned)B), dim3(256), 0, s>>>(w.objpart, (int)w.n_assign_blocks,
+  objective_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(w.objpart, (int)w.n_assign_blocks,
                                                            iters, t, objective);
   return hipGetLastError();
 }

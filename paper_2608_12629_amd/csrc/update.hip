@@ -30,10 +30,16 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ i
   const int i0 = ch * SORT_WC;
   const int i1 = min(N, i0 + SORT_WC);
   const int32_t* ib = idx + (size_t)b * N;
-  for (int i = i0 + threadIdx.x; i < i1; i += 256) {
-    const int k = ib[i];
-    if ((unsigned)k < (unsigned)K) atomicAdd(&cnt[k], 1);  // out-of-range ids are ignored
+  constexpr int PER = SORT_WC / 256;
+  int keys[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int i = i0 + u * 256 + (int)threadIdx.x;
+    keys[u] = i < i1 ? ib[i] : -1;
   }
+#pragma unroll
+  for (int u = 0; u < PER; ++u)
+    if ((unsigned)keys[u] < (unsigned)K) atomicAdd(&cnt[keys[u]], 1);  // out-of-range ids are ignored
   __syncthreads();
   int32_t* out = H + ((size_t)b * nch + ch) * K;
   for (int k = threadIdx.x; k < K; k += 256) out[k] = cnt[k];
@@ -47,6 +53,7 @@ __global__ __launch_bounds__(256) void colsum_kernel(const int32_t* __restrict__
   const int c0 = s * SORT_SEG, c1 = min(nch, c0 + SORT_SEG);
   const int32_t* h = H + (size_t)b * nch * K + k;
   int sum = 0;
+#pragma unroll 8
   for (int c = c0; c < c1; ++c) sum += h[(size_t)c * K];
   T[((size_t)b * nseg + s) * K + k] = sum;
 }
@@ -58,10 +65,15 @@ __global__ __launch_bounds__(256) void colscan_kernel(int32_t* __restrict__ T, i
   if (k >= K) return;
   int32_t* t = T + (size_t)b * nseg * K + k;
   int run = 0;
-  for (int s = 0; s < nseg; ++s) {
-    const int v = t[(size_t)s * K];
-    t[(size_t)s * K] = run;
-    run += v;
+  for (int s0 = 0; s0 < nseg; s0 += 16) {   // 16 independent loads in flight
+    int v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = s0 + u < nseg ? t[(size_t)(s0 + u) * K] : 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (s0 + u < nseg) t[(size_t)(s0 + u) * K] = run;
+      run += v[u];
+    }
   }
   counts[(size_t)b * K + k] = run;
 }
@@ -103,35 +115,60 @@ __global__ __launch_bounds__(256) void downsweep_kernel(int32_t* __restrict__ H,
   int base = off[(size_t)b * (K + 1) + k] + T[((size_t)b * nseg + s) * K + k];
   const int c0 = s * SORT_SEG, c1 = min(nch, c0 + SORT_SEG);
   int32_t* h = H + (size_t)b * nch * K + k;
-  for (int c = c0; c < c1; ++c) {
-    const int v = h[(size_t)c * K];
-    h[(size_t)c * K] = base;
-    base += v;
+  int v[SORT_SEG];
+#pragma unroll
+  for (int u = 0; u < SORT_SEG; ++u) v[u] = c0 + u < c1 ? h[(size_t)(c0 + u) * K] : 0;
+#pragma unroll
+  for (int u = 0; u < SORT_SEG; ++u) {
+    if (c0 + u < c1) h[(size_t)(c0 + u) * K] = base;
+    base += v[u];
   }
 }
 
 // One wave per chunk: points are taken 64 at a time in index order; lanes
 // that share a cluster id find each other with one ballot per key bit, rank
 // themselves by lane order, and the first of them advances the LDS cursor.
+// The chunk's ids are loaded into registers up front, so no step waits on
+// global memory.
 __global__ __launch_bounds__(64) void scatter_kernel(const int32_t* __restrict__ idx,
                                                      const int32_t* __restrict__ P, int N, int K,
                                                      int nch, int nbits,
                                                      int32_t* __restrict__ perm) {
+  constexpr int STEPS = SORT_WC / 64;
   extern __shared__ int32_t cur[];
   const int b = blockIdx.y, ch = blockIdx.x;
   const int lane = threadIdx.x;
-  const int32_t* p = P + ((size_t)b * nch + ch) * K;
-  for (int k = lane; k < K; k += 64) cur[k] = p[k];
-  __syncthreads();
   const int32_t* ib = idx + (size_t)b * N;
   int32_t* pb = perm + (size_t)b * N;
   const int i0 = ch * SORT_WC;
   const int i1 = min(N, i0 + SORT_WC);
+  int keys[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+    const int i = i0 + s * 64 + lane;
+    keys[s] = i < i1 ? ib[i] : -1;
+  }
+  // this chunk's run starts: K ints, copied 16 loads in flight at a time
+  const int32_t* p = P + ((size_t)b * nch + ch) * K;
+  for (int k0 = 0; k0 < K; k0 += 16 * 64) {
+    int v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int k = k0 + u * 64 + lane;
+      v[u] = k < K ? p[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int k = k0 + u * 64 + lane;
+      if (k < K) cur[k] = v[u];
+    }
+  }
+  __syncthreads();
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int base_i = i0; base_i < i1; base_i += 64) {
-    const int i = base_i + lane;
-    const int raw = i < i1 ? ib[i] : -1;
-    const bool valid = (unsigned)raw < (unsigned)K;  // out-of-range ids are ignored
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+    const int raw = keys[s];
+    const bool valid = (unsigned)raw < (unsigned)K;  // out-of-range ids (and the tail) are ignored
     const int key = valid ? raw : 0;
     uint64_t match = __ballot(valid);
     for (int bit = 0; bit < nbits; ++bit) {
@@ -143,7 +180,7 @@ __global__ __launch_bounds__(64) void scatter_kernel(const int32_t* __restrict__
       const int rank = __popcll(match & below);
       const int start = cur[key];
       if (rank == 0) cur[key] = start + __popcll(match);
-      pb[start + rank] = i;
+      pb[start + rank] = i0 + s * 64 + lane;
     }
   }
 }
@@ -193,7 +230,7 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
   constexpr int D = RC * E;
   constexpr int RPW = 64 / LPR;
   constexpr int NA = CPLR * E;
-  constexpr int U = 4;  // rows in flight per lane
+  constexpr int U = 8;  // rows in flight per lane
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int b = blockIdx.y;
@@ -221,19 +258,31 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
     float acc[NA];
 #pragma unroll
     for (int a = 0; a < NA; ++a) acc[a] = 0.f;
+    // U rows in flight per lane; the row ids of the next group are fetched
+    // while the current group's rows are loading
+    int pid[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int jj = pos + r + u * RPW;
+      pid[u] = jj < seg_end ? pb[jj] : -1;
+    }
     for (int j = pos + r; j < seg_end; j += U * RPW) {
       uint4 v[U][CPLR];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int jj = j + u * RPW;
-        if (jj < seg_end) {
-          const uint4* row = xb + (size_t)pb[jj] * RC + q * CPLR;
+        if (pid[u] >= 0) {
+          const uint4* row = xb + (size_t)pid[u] * RC + q * CPLR;
 #pragma unroll
           for (int c = 0; c < CPLR; ++c) v[u][c] = row[c];
         } else {
 #pragma unroll
           for (int c = 0; c < CPLR; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
         }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jj = j + (U + u) * RPW;
+        pid[u] = jj < seg_end ? pb[jj] : -1;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u)
