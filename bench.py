@@ -22,7 +22,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "Lloyd iter/s; assign TFLOP/s as % of MFMA peak at N=8M D=128 K=4096"
-PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16 MFMA (no sparsity)
+PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16/fp16 MFMA (no sparsity)
+PEAK_F32_TFLOPS = 157.3            # MI355X fp32 MFMA
 PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "assign_traffic.json")
 ASSIGN_SRC = os.path.join(ROOT, "paper_2608_12629_amd", "csrc", "assign.hip")
@@ -76,11 +77,13 @@ def cpu_baseline(w, sample_rows: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=None, help="default: the workload's iterations")
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--kernel-reps", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=1 << 20)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--workload", type=int, default=3,
+                    help="1..5; 3 (N=8M, D=128, K=4096) is the metric workload")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -92,13 +95,15 @@ def main():
     from paper_2608_12629_amd.synth import make_workload
 
     t0 = time.perf_counter()
-    w = make_workload(3)
+    w = make_workload(args.workload)
     log(f"workload {w.name} generated in {time.perf_counter() - t0:.1f} s")
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     X = w.X.to(dev)
     C0 = w.C0.to(dev)
     B, N, D, K = w.B, w.N, w.D, w.K
+    if args.steps is None:
+        args.steps = w.iters
     ws = km.Workspace(B, N, D, K, X.dtype, dev)
     C = C0.clone()
     idx = torch.empty((B, N), dtype=torch.int32, device=dev)
@@ -131,6 +136,7 @@ def main():
     flops = 2.0 * B * N * K * D
     assign_tflops = flops / (assign_ms * 1e-3) / 1e12
     upd_bytes = B * N * D * X.element_size() + 4 * B * N + 4 * B * K * D + 4 * B * K
+    peak = PEAK_BF16_TFLOPS if w.dtype != "f32" else PEAK_F32_TFLOPS
     upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9
     log(f"assign {assign_ms:.3f} ms = {assign_tflops:.1f} TFLOP/s; "
         f"update {update_ms:.3f} ms = {upd_gbs:.0f} GB/s algorithmic")
@@ -146,13 +152,13 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": {"bf16": "bf16", "f16": "f16", "f32": "f32"}[w.dtype],
         "data": "synthetic",
-        "config": {"workload": w.name, "B": B, "N": N, "D": D, "K": K, "x_dtype": "bf16",
+        "config": {"workload": w.name, "B": B, "N": N, "D": D, "K": K, "x_dtype": w.dtype,
                    "centroid_dtype": "f32", "iters_per_step": 1},
         "roofline": {"bound": "mfma", "kernel": "assign", "achieved": assign_tflops,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": assign_tflops / PEAK_BF16_TFLOPS, "traffic": stored_traffic()},
+                     "peak": peak, "unit": "TFLOP/s",
+                     "frac": assign_tflops / peak, "traffic": stored_traffic()},
         "update": {"ms": update_ms, "algorithmic_bytes": upd_bytes, "GB/s": upd_gbs,
                    "hbm_frac": upd_gbs / PEAK_HBM_GBS},
         "assign_ms": assign_ms,

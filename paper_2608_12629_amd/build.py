@@ -12,7 +12,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libflashkmeans.so")
-SOURCES = ["api.hip", "assign.hip", "update.hip"]
+SOURCES = ["api.hip", "assign.hip", "assign_tiled.hip", "update.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -14,8 +14,12 @@ static size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
   Workspace w{};
-  const int64_t ppb = assign_points_per_block(dt, D);
-  w.n_assign_blocks = (N + ppb - 1) / ppb;
+  if (assign_tiled(dt, D)) {
+    w.n_assign_blocks = (N + 255) / 256;  // the decode kernel's blocks
+  } else {
+    const int64_t ppb = assign_points_per_block(dt, D);
+    w.n_assign_blocks = (N + ppb - 1) / ppb;
+  }
   w.n_sort_chunks = (N + SORT_WC - 1) / SORT_WC;
   w.n_seg = (w.n_sort_chunks + SORT_SEG - 1) / SORT_SEG;
   w.n_red_chunks = (N + RED_CR - 1) / RED_CR;
@@ -36,6 +40,9 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   w.perm = (int32_t*)take((size_t)(B * N) * 4);
   w.carry = (float*)take((size_t)(B * w.n_red_chunks * 2 * D) * 4);
   w.sums = (float*)take((size_t)(B * K * D) * 4);
+  const bool tiled = assign_tiled(dt, D);
+  w.keys = (uint64_t*)take(tiled ? (size_t)(B * N) * 8 : 0);
+  w.xnorm = (float*)take(tiled ? (size_t)(B * N) * 4 : 0);
   w.total = o;
   return w;
 }
@@ -47,7 +54,7 @@ static int check_sizes(int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
   if (B < 1 || N < 1 || D < 1 || K < 1) return FKM_ERR_INVALID_ARG;
   if (dt != DT_F32 && dt != DT_BF16 && dt != DT_F16) return FKM_ERR_INVALID_ARG;
   if (N > INT32_MAX || K > MAX_K || D > MAX_D || B > 65535) return FKM_ERR_UNSUPPORTED;
-  if (!row_bytes_ok(dt, D) || !assign_resident_ok(dt, D)) return FKM_ERR_UNSUPPORTED;
+  if (!row_bytes_ok(dt, D) || !assign_ok(dt, D)) return FKM_ERR_UNSUPPORTED;
   return FKM_OK;
 }
 

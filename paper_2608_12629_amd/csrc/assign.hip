@@ -17,85 +17,9 @@
 // it receives accumulator rows 4 g .. 4 g + 3 of column m.  A lane therefore
 // keeps a running best over its own quarter of the centroids of one point,
 // and the four quarters are merged once at the end.
-#include "fkm_internal.h"
+#include "fkm_device.h"
 
 namespace fkm {
-
-// ---------------------------------------------------------------------------
-// element helpers
-template <int DT> struct Elem;
-template <> struct Elem<DT_BF16> {
-  static constexpr int per16 = 8;  // elements in 16 bytes
-  __device__ static float widen(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-  __device__ static uint16_t narrow(float f) {
-    __bf16 b = (__bf16)f;  // round to nearest even
-    return __builtin_bit_cast(uint16_t, b);
-  }
-};
-template <> struct Elem<DT_F16> {
-  static constexpr int per16 = 8;
-  __device__ static float widen(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
-  __device__ static uint16_t narrow(float f) {
-    _Float16 b = (_Float16)f;  // round to nearest even
-    return __builtin_bit_cast(uint16_t, b);
-  }
-};
-template <> struct Elem<DT_F32> {
-  static constexpr int per16 = 4;
-};
-
-// Sum of squares of the elements of one 16-byte chunk, widened to fp32,
-// accumulated in element order.
-template <int DT>
-__device__ inline float chunk_sumsq(const uint4& q, float acc) {
-  if constexpr (DT == DT_F32) {
-    const float v[4] = {__uint_as_float(q.x), __uint_as_float(q.y), __uint_as_float(q.z),
-                        __uint_as_float(q.w)};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc = __builtin_fmaf(v[e], v[e], acc);
-  } else {
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = Elem<DT>::widen((uint16_t)(w[e] & 0xffffu));
-      const float hi = Elem<DT>::widen((uint16_t)(w[e] >> 16));
-      acc = __builtin_fmaf(lo, lo, acc);
-      acc = __builtin_fmaf(hi, hi, acc);
-    }
-  }
-  return acc;
-}
-
-// acc += A-chunk x B-chunk over the k-slice these two 16-byte chunks carry.
-template <int DT>
-__device__ inline f32x4 mfma_chunk(const uint4& a, const uint4& b, f32x4 acc) {
-  if constexpr (DT == DT_BF16) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-  } else if constexpr (DT == DT_F16) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
-                                                  __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
-  } else {
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
-    return acc;
-  }
-}
-
-
-// acc += A-chunk x B-chunk on a 32x32x16 tile (16-bit storage types).
-template <int DT>
-__device__ inline f32x16 mfma32_chunk(const uint4& a, const uint4& b, f32x16 acc) {
-  if constexpr (DT == DT_BF16) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-  } else {
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
-                                                  __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // prep: c^ = round(c) to the storage type and cinit = -|c^|^2 / 2 (fp32),
@@ -656,6 +580,7 @@ static hipError_t launch_pipe_dt(const void* X, const Workspace& w, int64_t B, i
 
 hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
+  if (assign_tiled(dt, D)) return launch_assign_tiled(X, dt, w, B, N, D, idx, min_dist, s);
   if (!assign_resident_ok(dt, D)) return hipErrorInvalidValue;
   if (dt == DT_BF16) return launch_pipe_dt<DT_BF16>(X, w, B, N, D, idx, min_dist, s);
   if (dt == DT_F16) return launch_pipe_dt<DT_F16>(X, w, B, N, D, idx, min_dist, s);

@@ -26,7 +26,7 @@ constexpr int ASSIGN_THREADS = 256;
 constexpr int ASSIGN_TCS = 64;
 // The rounded centroids and their norms are stored padded to a whole number of
 // ASSIGN_KPAD-row stages: padding rows are zero with the most negative score.
-constexpr int ASSIGN_KPAD = 64;
+constexpr int ASSIGN_KPAD = 128;
 inline int64_t kpad(int64_t K) { return (K + ASSIGN_KPAD - 1) / ASSIGN_KPAD * ASSIGN_KPAD; }
 // Update: the counting sort works on chunks of SORT_WC points (one wave ranks
 // a chunk); chunk histograms are scanned in segments of SORT_SEG chunks; the
@@ -55,11 +55,16 @@ inline int64_t assign_points_per_block(int dt, int64_t D) {
   return 4 * 16 * (D * 4 / 64 <= 4 ? 8 : 4);
 }
 
-// The resident-X assignment kernel handles these row widths (bytes per point).
+// The resident-X assignment kernels handle these row widths (bytes per point);
+// wider 16-bit rows go to the tiled kernel.
 inline bool assign_resident_ok(int dt, int64_t D) {
   const int64_t rb = D * dt_bytes(dt);
   return rb == 64 || rb == 128 || rb == 256 || rb == 512;
 }
+inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D >= 512; }
+inline bool assign_ok(int dt, int64_t D) { return assign_resident_ok(dt, D) || assign_tiled(dt, D); }
+// Tiled kernel: 128-point x 128-centroid tiles, TILED_CBG centroid blocks per workgroup.
+constexpr int TILED_BP = 128, TILED_BC = 128, TILED_CBG = 8;
 
 // ---- workspace layout -------------------------------------------------------
 struct Workspace {
@@ -72,6 +77,8 @@ struct Workspace {
   int32_t* perm;   // [B,N] point ids sorted by cluster
   float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by chunk ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
+  uint64_t* keys;  // [B,N] best (score, index) of each point (tiled assignment only)
+  float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
   int64_t Kp, n_assign_blocks, n_sort_chunks, n_seg, n_red_chunks;
   size_t total;
 };
@@ -83,6 +90,8 @@ hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp,
                        void* chat, float* cinit, hipStream_t s);
 hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
+                               int64_t D, int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
                             hipStream_t s);
 hipError_t update_init();

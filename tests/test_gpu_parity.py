@@ -72,6 +72,7 @@ SMALL = {
     "cfg2_small": dict(cfg=2, N=65536, K=256),
     "cfg3_small": dict(cfg=3, N=65536, K=512),
     "cfg4_small": dict(cfg=4, B=8, N=4096),
+    "cfg5_small": dict(cfg=5, N=20000, K=700),
 }
 
 
@@ -89,7 +90,7 @@ def test_cfg4_full_teacher_forced(km, oracle):
     teacher_forced(km, oracle, w.X, w.C0, w.dtype, 3)
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
+@pytest.mark.parametrize("cfg", [2, 3, 5])
 def test_full_size_sampled(km, oracle, cfg):
     """Full-size workload: assignment checked on 4096 sampled rows, update in full."""
     w = make_workload(cfg)
@@ -124,6 +125,9 @@ SHAPES = [
     (1, 3000, 32, 65, "bf16"),        # D = 32
     (3, 2500, 64, 40, "f16"),         # batched, ragged
     (1, 300, 64, 300, "bf16"),        # K = N
+    (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
+    (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
+    (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
 ]
 
 
