@@ -82,6 +82,8 @@ def main():
     ap.add_argument("--kernel-reps", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=1 << 20)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--workload", type=int, default=3,
                     help="1..5; 3 (N=8M, D=128, K=4096) is the metric workload")
     args = ap.parse_args()
@@ -109,6 +111,13 @@ def main():
     idx = torch.empty((B, N), dtype=torch.int32, device=dev)
     md = torch.empty((B, N), dtype=torch.float32, device=dev)
     cnt = torch.empty((B, K), dtype=torch.int32, device=dev)
+
+    if args.calib_copy_mib:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # warm-up, then exactly `steps` Lloyd iterations from C0
     km.kmeans_lloyd(X, C, args.warmup, idx=idx, min_dist=md, counts=cnt, ws=ws)
