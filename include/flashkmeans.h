@@ -31,7 +31,7 @@
  * - Errors: arguments are validated on the host before anything is enqueued;
  *   a rejected call returns a negative status and has no effect.
  *   FKM_ERR_UNSUPPORTED means valid but outside what this build implements
- *   (not gfx950, D not a multiple of 32, D > 2048, K > 32768, N > 2^31-1).
+ *   (not gfx950, D not a multiple of 32, D > 2048, K > 65536, N > 2^31-1).
  *   FKM_ERR_HIP reports a failed HIP call or launch.  No C++ exception
  *   crosses this boundary.
  */

@@ -20,8 +20,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
     const int64_t ppb = assign_points_per_block(dt, D);
     w.n_assign_blocks = (N + ppb - 1) / ppb;
   }
-  w.n_sort_chunks = (N + SORT_WC - 1) / SORT_WC;
-  w.n_seg = (w.n_sort_chunks + SORT_SEG - 1) / SORT_SEG;
+  w.n_sort_chunks = (N + RADIX_CHUNK - 1) / RADIX_CHUNK;
   w.n_red_chunks = (N + RED_CR - 1) / RED_CR;
   char* p = (char*)base;
   size_t o = 0;
@@ -34,8 +33,12 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
   w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
   w.objpart = (double*)take((size_t)(B * w.n_assign_blocks) * 8);
-  w.hist = (int32_t*)take((size_t)(B * w.n_sort_chunks * K) * 4);
-  w.segsum = (int32_t*)take((size_t)(B * w.n_seg * K) * 4);
+  w.rhist = (int32_t*)take((size_t)(B * RADIX_MAX_R * w.n_sort_chunks) * 4);
+  w.rbin = (int32_t*)take((size_t)B * RADIX_MAX_R * 4);
+  w.rtotal = (int32_t*)take((size_t)B * 4);
+  w.keys_a = (int32_t*)take((size_t)(B * N) * 4);
+  w.vals_a = (int32_t*)take((size_t)(B * N) * 4);
+  w.keys_b = (int32_t*)take((size_t)(B * N) * 4);
   w.off = (int32_t*)take((size_t)(B * (K + 1)) * 4);
   w.perm = (int32_t*)take((size_t)(B * N) * 4);
   w.carry = (float*)take((size_t)(B * w.n_red_chunks * 2 * D) * 4);

@@ -28,14 +28,15 @@ constexpr int ASSIGN_TCS = 64;
 // ASSIGN_KPAD-row stages: padding rows are zero with the most negative score.
 constexpr int ASSIGN_KPAD = 128;
 inline int64_t kpad(int64_t K) { return (K + ASSIGN_KPAD - 1) / ASSIGN_KPAD * ASSIGN_KPAD; }
-// Update: the counting sort works on chunks of SORT_WC points (one wave ranks
-// a chunk); chunk histograms are scanned in segments of SORT_SEG chunks; the
-// segmented sum gives each wave RED_CR consecutive entries of the sorted order.
-constexpr int SORT_WC = 4096;
-constexpr int SORT_SEG = 32;
+// Update: the radix sort works on chunks of RADIX_CHUNK entries with digits of
+// at most RADIX_MAX_BITS bits; the segmented sum gives each wave RED_CR
+// consecutive entries of the sorted order.
+constexpr int RADIX_CHUNK = 4096;
+constexpr int RADIX_MAX_BITS = 8;
+constexpr int RADIX_MAX_R = 1 << RADIX_MAX_BITS;
 constexpr int RED_CR = 2048;
 // Limits of this build.
-constexpr int64_t MAX_K = 32768;   // LDS counters of the counting sort
+constexpr int64_t MAX_K = 65536;   // two radix passes of at most 8 bits
 constexpr int64_t MAX_D = 2048;
 
 // Row widths (bytes per point) the kernels handle: a power of two from 64 B
@@ -71,15 +72,19 @@ struct Workspace {
   void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad(K))
   float* cinit;    // [B,Kp]   -1/2 * squared norm of each rounded centroid
   double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
-  int32_t* hist;   // [B,n_sort_chunks,K] chunk histograms, then chunk start offsets
-  int32_t* segsum; // [B,n_seg,K] histogram sums per segment of chunks
+  int32_t* rhist;  // [B,R,n_sort_chunks] radix histograms, then run starts (R <= 256)
+  int32_t* rbin;   // [B,256] radix bin totals
+  int32_t* rtotal; // [B] number of valid entries (ids in [0, K))
+  int32_t* keys_a; // [B,N] cluster ids after the first radix pass
+  int32_t* vals_a; // [B,N] point ids after the first radix pass
+  int32_t* keys_b; // [B,N] cluster ids, sorted
   int32_t* off;    // [B,K+1] cluster start offsets in the sorted order
   int32_t* perm;   // [B,N] point ids sorted by cluster
   float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by chunk ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
   uint64_t* keys;  // [B,N] best (score, index) of each point (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
-  int64_t Kp, n_assign_blocks, n_sort_chunks, n_seg, n_red_chunks;
+  int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks;
   size_t total;
 };
 

@@ -3,186 +3,224 @@
 //
 // The paper calls this step bandwidth- and atomic-contention-sensitive.  Here
 // it uses no floating-point atomics and is deterministic:
-//   1. hist      per chunk of SORT_WC points, a histogram over the K clusters
-//   2. colsum    per segment of SORT_SEG chunks, the sum of those histograms
-//   3. colscan   per cluster, an exclusive scan over segments; the total is count_k
-//   4. kscan     per instance, an exclusive scan of the counts: cluster offsets
-//   5. downsweep per (chunk, cluster), the absolute start of that chunk's run
-//   6. scatter   one wave per chunk ranks its points in order (ballot
-//                multi-split) and writes them to their sorted slots: a stable
-//                counting sort of the point ids by cluster
-//   7. segreduce one wave per RED_CR consecutive sorted entries streams the
-//                whole rows X[perm[j]] and sums each cluster run in fp32 in a
-//                fixed order; a run cut by a chunk end leaves a partial
-//   8. finalize  per cluster, the sum (or its partials, in chunk order) over
-//                the count; an empty cluster keeps its previous centroid.
+//   1. a stable radix sort of the point ids by cluster id (one or two passes of
+//      histogram, scan and LDS-staged scatter; see below)
+//   2. bounds     per cluster, its run [off_k, off_k+1) in the sorted order
+//   3. segreduce  one wave per RED_CR consecutive sorted entries streams the
+//                 whole rows X[perm[j]] and sums each cluster run in fp32 in a
+//                 fixed order; a run cut by a chunk end leaves a partial
+//   4. finalize   per cluster, the sum (or its partials, in chunk order) over
+//                 the count; an empty cluster keeps its previous centroid.
 #include "fkm_internal.h"
 
 namespace fkm {
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ idx, int N, int K,
-                                                   int nch, int32_t* __restrict__ H) {
-  extern __shared__ int32_t cnt[];
-  const int b = blockIdx.y, ch = blockIdx.x;
-  for (int k = threadIdx.x; k < K; k += 256) cnt[k] = 0;
+// Stable LSD radix sort of (cluster id, point id) by cluster id: one pass per
+// digit of at most 8 bits (two passes for K <= 65536).  Each pass:
+//   radix_hist     per chunk of RADIX_CHUNK entries, a histogram over the R bins
+//   radix_scan     per bin, exclusive scan over chunks (+ the bin total); the
+//                  scatter adds the bin's start to get each (bin, chunk) run start
+//   radix_scatter  per chunk, four waves rank their quarters in entry order
+//                  (ballot multi-split), stage the chunk sorted by bin in LDS,
+//                  and write each bin's run out contiguously (coalesced)
+// Pass one reads the assignment itself and ignores ids outside [0, K).
+namespace {
+
+__device__ __forceinline__ int digit_of(int key, int shift, int R) { return (key >> shift) & (R - 1); }
+
+}  // namespace
+
+__global__ __launch_bounds__(256) void radix_hist_kernel(const int32_t* __restrict__ keys, int N,
+                                                         int K, const int32_t* __restrict__ total,
+                                                         int shift, int R, int nch,
+                                                         int32_t* __restrict__ H) {
+  __shared__ int cnt[RADIX_MAX_R];
+  const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
+  const int n_in = total ? total[b] : N;  // later passes read the valid prefix only
+  for (int r = t; r < R; r += 256) cnt[r] = 0;
   __syncthreads();
-  const int i0 = ch * SORT_WC;
-  const int i1 = min(N, i0 + SORT_WC);
-  const int32_t* ib = idx + (size_t)b * N;
-  constexpr int PER = SORT_WC / 256;
-  int keys[PER];
+  const int32_t* kb = keys + (size_t)b * N;
+  constexpr int PER = RADIX_CHUNK / 256;
+  int k[PER];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    const int i = i0 + u * 256 + (int)threadIdx.x;
-    keys[u] = i < i1 ? ib[i] : -1;
+    const int i = ch * RADIX_CHUNK + u * 256 + t;
+    k[u] = i < n_in ? kb[i] : -1;
   }
 #pragma unroll
   for (int u = 0; u < PER; ++u)
-    if ((unsigned)keys[u] < (unsigned)K) atomicAdd(&cnt[keys[u]], 1);  // out-of-range ids are ignored
+    if ((unsigned)k[u] < (unsigned)K) atomicAdd(&cnt[digit_of(k[u], shift, R)], 1);
   __syncthreads();
-  int32_t* out = H + ((size_t)b * nch + ch) * K;
-  for (int k = threadIdx.x; k < K; k += 256) out[k] = cnt[k];
+  for (int r = t; r < R; r += 256) H[((size_t)b * R + r) * nch + ch] = cnt[r];
 }
 
-__global__ __launch_bounds__(256) void colsum_kernel(const int32_t* __restrict__ H, int K, int nch,
-                                                     int nseg, int32_t* __restrict__ T) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int s = blockIdx.y, b = blockIdx.z;
-  if (k >= K) return;
-  const int c0 = s * SORT_SEG, c1 = min(nch, c0 + SORT_SEG);
-  const int32_t* h = H + (size_t)b * nch * K + k;
+// Per bin (one workgroup each): exclusive scan of the bin's chunk counts in
+// place, and the bin total into T[b][bin].  Bin starts are the exclusive scan
+// of T, done by each scatter workgroup on its own (R <= 256 values).
+__global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H, int R, int nch,
+                                                         int32_t* __restrict__ T) {
+  __shared__ int32_t part[256];
+  const int r = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  int32_t* h = H + ((size_t)b * R + r) * nch;
+  const int per = (nch + 255) / 256;
+  const int i0 = min(nch, t * per), i1 = min(nch, i0 + per);
+  int v[16];
   int sum = 0;
-#pragma unroll 8
-  for (int c = c0; c < c1; ++c) sum += h[(size_t)c * K];
-  T[((size_t)b * nseg + s) * K + k] = sum;
-}
-
-__global__ __launch_bounds__(256) void colscan_kernel(int32_t* __restrict__ T, int K, int nseg,
-                                                      int32_t* __restrict__ counts) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int b = blockIdx.y;
-  if (k >= K) return;
-  int32_t* t = T + (size_t)b * nseg * K + k;
-  int run = 0;
-  for (int s0 = 0; s0 < nseg; s0 += 16) {   // 16 independent loads in flight
-    int v[16];
+  for (int c0 = i0; c0 < i1; c0 += 16) {
 #pragma unroll
-    for (int u = 0; u < 16; ++u) v[u] = s0 + u < nseg ? t[(size_t)(s0 + u) * K] : 0;
+    for (int u = 0; u < 16; ++u) v[u] = c0 + u < i1 ? h[c0 + u] : 0;
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      if (s0 + u < nseg) t[(size_t)(s0 + u) * K] = run;
-      run += v[u];
-    }
+    for (int u = 0; u < 16; ++u) sum += v[u];
   }
-  counts[(size_t)b * K + k] = run;
-}
-
-// Exclusive scan of one instance's K counts into K+1 offsets (1024 threads).
-__global__ __launch_bounds__(1024) void kscan_kernel(const int32_t* __restrict__ counts, int K,
-                                                     int32_t* __restrict__ off) {
-  __shared__ int32_t part[1024];
-  const int b = blockIdx.x, t = threadIdx.x;
-  const int per = (K + 1023) / 1024;
-  const int k0 = min(K, t * per), k1 = min(K, k0 + per);
-  const int32_t* c = counts + (size_t)b * K;
-  int sum = 0;
-  for (int k = k0; k < k1; ++k) sum += c[k];
   part[t] = sum;
   __syncthreads();
-  for (int w = 1; w < 1024; w <<= 1) {  // Hillis-Steele inclusive scan
-    const int v = t >= w ? part[t - w] : 0;
+  for (int w = 1; w < 256; w <<= 1) {
+    const int a = t >= w ? part[t - w] : 0;
     __syncthreads();
-    part[t] += v;
+    part[t] += a;
     __syncthreads();
   }
   int run = part[t] - sum;
-  int32_t* o = off + (size_t)b * (K + 1);
-  for (int k = k0; k < k1; ++k) {
-    o[k] = run;
-    run += c[k];
+  for (int c0 = i0; c0 < i1; c0 += 16) {
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = c0 + u < i1 ? h[c0 + u] : 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (c0 + u < i1) h[c0 + u] = run;
+      run += v[u];
+    }
   }
-  if (t == 1023) o[K] = part[1023];
+  if (t == 255) T[(size_t)b * RADIX_MAX_R + r] = part[255];
 }
 
-__global__ __launch_bounds__(256) void downsweep_kernel(int32_t* __restrict__ H,
-                                                        const int32_t* __restrict__ T,
-                                                        const int32_t* __restrict__ off, int K,
-                                                        int nch, int nseg) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int s = blockIdx.y, b = blockIdx.z;
-  if (k >= K) return;
-  int base = off[(size_t)b * (K + 1) + k] + T[((size_t)b * nseg + s) * K + k];
-  const int c0 = s * SORT_SEG, c1 = min(nch, c0 + SORT_SEG);
-  int32_t* h = H + (size_t)b * nch * K + k;
-  int v[SORT_SEG];
-#pragma unroll
-  for (int u = 0; u < SORT_SEG; ++u) v[u] = c0 + u < c1 ? h[(size_t)(c0 + u) * K] : 0;
-#pragma unroll
-  for (int u = 0; u < SORT_SEG; ++u) {
-    if (c0 + u < c1) h[(size_t)(c0 + u) * K] = base;
-    base += v[u];
-  }
-}
+__global__ __launch_bounds__(256) void radix_scatter_kernel(
+    const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int N, int K,
+    const int32_t* __restrict__ total, int shift, int dbits, int nch,
+    const int32_t* __restrict__ H, const int32_t* __restrict__ T, int32_t* __restrict__ total_out,
+    int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
+  constexpr int STEPS = RADIX_CHUNK / 256;  // 64-entry steps per wave
+  __shared__ int skey[RADIX_CHUNK], sval[RADIX_CHUNK];
+  __shared__ int cur[4][RADIX_MAX_R];
+  __shared__ int lstart[RADIX_MAX_R + 1], gstart[RADIX_MAX_R], bstart[RADIX_MAX_R + 1];
+  const int R = 1 << dbits;
+  const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
+  const int lane = t & 63, w = t >> 6;
+  const int n_in = total ? total[b] : N;
+  const int32_t* kb = keys_in + (size_t)b * N;
+  const int32_t* vb = vals_in ? vals_in + (size_t)b * N : nullptr;
+  const int ibase = ch * RADIX_CHUNK + w * (RADIX_CHUNK / 4);
 
-// One wave per chunk: points are taken 64 at a time in index order; lanes
-// that share a cluster id find each other with one ballot per key bit, rank
-// themselves by lane order, and the first of them advances the LDS cursor.
-// The chunk's ids are loaded into registers up front, so no step waits on
-// global memory.
-__global__ __launch_bounds__(64) void scatter_kernel(const int32_t* __restrict__ idx,
-                                                     const int32_t* __restrict__ P, int N, int K,
-                                                     int nch, int nbits,
-                                                     int32_t* __restrict__ perm) {
-  constexpr int STEPS = SORT_WC / 64;
-  extern __shared__ int32_t cur[];
-  const int b = blockIdx.y, ch = blockIdx.x;
-  const int lane = threadIdx.x;
-  const int32_t* ib = idx + (size_t)b * N;
-  int32_t* pb = perm + (size_t)b * N;
-  const int i0 = ch * SORT_WC;
-  const int i1 = min(N, i0 + SORT_WC);
-  int keys[STEPS];
+  int k[STEPS], v[STEPS];
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    const int i = i0 + s * 64 + lane;
-    keys[s] = i < i1 ? ib[i] : -1;
+    const int i = ibase + s * 64 + lane;
+    const bool in = i < n_in;
+    k[s] = in ? kb[i] : -1;
+    v[s] = in ? (vb ? vb[i] : i) : 0;
   }
-  // this chunk's run starts: K ints, copied 16 loads in flight at a time
-  const int32_t* p = P + ((size_t)b * nch + ch) * K;
-  for (int k0 = 0; k0 < K; k0 += 16 * 64) {
-    int v[16];
+  for (int r = t; r < 4 * RADIX_MAX_R; r += 256) (&cur[0][0])[r] = 0;
+  // bin starts: exclusive scan of the bin totals
+  if (t < RADIX_MAX_R) bstart[t + 1] = t < R ? T[(size_t)b * RADIX_MAX_R + t] : 0;
+  if (t == 0) bstart[0] = 0;
+  __syncthreads();
+  for (int d = 1; d <= RADIX_MAX_R; d <<= 1) {
+    int add = 0;
+    if (t < RADIX_MAX_R && t + 1 > d) add = bstart[t + 1 - d];
+    __syncthreads();
+    if (t < RADIX_MAX_R) bstart[t + 1] += add;
+    __syncthreads();
+  }
+  if (total_out && ch == 0 && t == 0) total_out[b] = bstart[RADIX_MAX_R];
+  // per-wave bin counts (integer atomics: exact)
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int k = k0 + u * 64 + lane;
-      v[u] = k < K ? p[k] : 0;
+  for (int s = 0; s < STEPS; ++s)
+    if ((unsigned)k[s] < (unsigned)K) atomicAdd(&cur[w][digit_of(k[s], shift, R)], 1);
+  __syncthreads();
+  // chunk totals per bin -> exclusive scan over bins (lstart); wave starts per bin
+  if (t < RADIX_MAX_R) {
+    int tot = 0;
+    if (t < R) {
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) tot += cur[ww][t];
+      gstart[t] = bstart[t] + H[((size_t)b * R + t) * nch + ch];
     }
+    lstart[t + 1] = tot;
+  }
+  if (t == 0) lstart[0] = 0;
+  __syncthreads();
+  for (int d = 1; d <= RADIX_MAX_R; d <<= 1) {  // inclusive scan of lstart[1..R]
+    int add = 0;
+    if (t < RADIX_MAX_R && t + 1 > d) add = lstart[t + 1 - d];
+    __syncthreads();
+    if (t < RADIX_MAX_R) lstart[t + 1] += add;
+    __syncthreads();
+  }
+  if (t < R) {
+    int run = lstart[t];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int k = k0 + u * 64 + lane;
-      if (k < K) cur[k] = v[u];
+    for (int ww = 0; ww < 4; ++ww) {
+      const int c = cur[ww][t];
+      cur[ww][t] = run;
+      run += c;
     }
   }
   __syncthreads();
+  // rank in entry order within each wave and stage the chunk sorted by bin
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    const int raw = keys[s];
-    const bool valid = (unsigned)raw < (unsigned)K;  // out-of-range ids (and the tail) are ignored
-    const int key = valid ? raw : 0;
+    const bool valid = (unsigned)k[s] < (unsigned)K;
+    const int dg = valid ? digit_of(k[s], shift, R) : 0;
     uint64_t match = __ballot(valid);
-    for (int bit = 0; bit < nbits; ++bit) {
-      const bool on = (key >> bit) & 1;
+    for (int bit = 0; bit < dbits; ++bit) {
+      const bool on = (dg >> bit) & 1;
       const uint64_t bb = __ballot(valid && on);
       match &= on ? bb : ~bb;
     }
     if (valid) {
       const int rank = __popcll(match & below);
-      const int start = cur[key];
-      if (rank == 0) cur[key] = start + __popcll(match);
-      pb[start + rank] = i0 + s * 64 + lane;
+      const int start = cur[w][dg];
+      if (rank == 0) cur[w][dg] = start + __popcll(match);
+      skey[start + rank] = k[s];
+      sval[start + rank] = v[s];
     }
   }
+  __syncthreads();
+  // write each bin's run contiguously
+  const int nloc = lstart[R];
+  int32_t* ko = keys_out ? keys_out + (size_t)b * N : nullptr;
+  int32_t* vo = vals_out + (size_t)b * N;
+  for (int j = t; j < nloc; j += 256) {
+    const int key = skey[j];
+    const int dg = digit_of(key, shift, R);
+    const int g = gstart[dg] + (j - lstart[dg]);
+    if (ko) ko[g] = key;
+    vo[g] = sval[j];
+  }
+}
+
+// Cluster offsets and counts from the sorted keys: off[k] = first position of
+// a key >= k (binary search), count_k = off[k+1] - off[k].
+__global__ __launch_bounds__(256) void bounds_kernel(const int32_t* __restrict__ sorted,
+                                                     const int32_t* __restrict__ total, int N, int K,
+                                                     int32_t* __restrict__ off,
+                                                     int32_t* __restrict__ counts) {
+  const int k = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+  if (k > K) return;
+  const int n = total[b];
+  const int32_t* s = sorted + (size_t)b * N;
+  auto lower = [&](int key) {
+    int lo = 0, hi = n;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+  };
+  const int a = lower(k);
+  off[(size_t)b * (K + 1) + k] = a;
+  if (k < K) counts[(size_t)b * K + k] = lower(k + 1) - a;
 }
 
 // ---------------------------------------------------------------------------
@@ -401,38 +439,53 @@ static hipError_t launch_segreduce_dt(const void* X, const Workspace& w, int64_t
   return hipGetLastError();
 }
 
-hipError_t update_init() {
-  // The histogram and scatter kernels keep K int32 counters in dynamic LDS.
-  const int bytes = 4 * MAX_K;
-  hipError_t e = hipFuncSetAttribute((const void*)hist_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)scatter_kernel,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+hipError_t update_init() { return hipSuccess; }
+
+// Digit widths: the key needs `bits` bits; one pass for <= 8 bits, else two
+// passes of about half each.
+static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
+  int bits = 1;
+  while ((1ll << bits) < K) ++bits;
+  passes = bits <= RADIX_MAX_BITS ? 1 : 2;
+  d1 = passes == 1 ? bits : (bits + 1) / 2;
+  d2 = bits - (passes == 1 ? 0 : d1);
 }
 
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
                          float* C_out, int32_t* counts, hipStream_t s) {
   hipError_t e;
-  const int nch = (int)w.n_sort_chunks, nseg = (int)w.n_seg;
-  const unsigned kb = (unsigned)((K + 255) / 256);
-  hist_kernel<<<dim3(nch, (unsigned)B), 256, K * sizeof(int32_t), s>>>(idx, (int)N, (int)K, nch,
-                                                                      w.hist);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  colsum_kernel<<<dim3(kb, nseg, (unsigned)B), 256, 0, s>>>(w.hist, (int)K, nch, nseg, w.segsum);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  colscan_kernel<<<dim3(kb, (unsigned)B), 256, 0, s>>>(w.segsum, (int)K, nseg, counts);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  kscan_kernel<<<dim3((unsigned)B), 1024, 0, s>>>(counts, (int)K, w.off);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  downsweep_kernel<<<dim3(kb, nseg, (unsigned)B), 256, 0, s>>>(w.hist, w.segsum, w.off, (int)K,
-                                                               nch, nseg);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  int nbits = 0;
-  while ((1ll << nbits) < K) ++nbits;
-  scatter_kernel<<<dim3(nch, (unsigned)B), 64, K * sizeof(int32_t), s>>>(idx, w.hist, (int)N,
-                                                                        (int)K, nch, nbits, w.perm);
+  const int nch = (int)w.n_sort_chunks;
+  int passes, d1, d2;
+  radix_plan(K, passes, d1, d2);
+  // pass 1: idx (raw) -> (keys_a, vals_a) sorted by the low digit; with one
+  // pass the values go straight to perm and the keys to keys_b
+  {
+    const int R = 1 << d1;
+    radix_hist_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(idx, (int)N, (int)K, nullptr, 0, R, nch,
+                                                            w.rhist);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scatter_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(
+        idx, nullptr, (int)N, (int)K, nullptr, 0, d1, nch, w.rhist, w.rbin, w.rtotal,
+        passes == 1 ? w.keys_b : w.keys_a, passes == 1 ? w.perm : w.vals_a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (passes == 2) {
+    const int R = 1 << d2;
+    radix_hist_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(w.keys_a, (int)N, (int)K, w.rtotal, d1,
+                                                            R, nch, w.rhist);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scatter_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(
+        w.keys_a, w.vals_a, (int)N, (int)K, w.rtotal, d1, d2, nch, w.rhist, w.rbin, nullptr,
+        w.keys_b, w.perm);  // the second pass keeps the same total
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  bounds_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
+      w.keys_b, w.rtotal, (int)N, (int)K, w.off, counts);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (dt == DT_BF16) e = launch_segreduce_dt<DT_BF16>(X, w, B, N, D, K, s);
   else if (dt == DT_F16) e = launch_segreduce_dt<DT_F16>(X, w, B, N, D, K, s);

@@ -63,7 +63,7 @@ def test_workspace_bytes(lib):
         assert cur >= prev
         prev = cur
     prev = 0
-    for K in (1, 7, 64, 1000, 4096, 32768):
+    for K in (1, 7, 64, 1000, 4096, 32768, 65536):
         cur = ws(1, 65536, 64, K)
         assert cur >= prev
         prev = cur
@@ -71,7 +71,7 @@ def test_workspace_bytes(lib):
     # rejected shapes report 0
     assert ws(0, 10, 64, 4) == 0 and ws(1, 0, 64, 4) == 0 and ws(1, 10, 64, 0) == 0
     assert ws(1, 10, 48, 4) == 0            # D not a multiple of 32
-    assert ws(1, 10, 64, 40000) == 0        # K above the counting-sort limit
+    assert ws(1, 10, 64, 70000) == 0        # K above the sort limit
     assert ws(1, 10, 64, 4, 7) == 0         # unknown dtype
 
 
@@ -105,7 +105,7 @@ def test_rejections_before_any_device_call(lib, call):
     assert call(lib, D=0) == EINVAL
     assert call(lib, D=48) == EUNSUP
     assert call(lib, D=4096) == EUNSUP
-    assert call(lib, K=40000) == EUNSUP
+    assert call(lib, K=70000) == EUNSUP
     assert call(lib, N=1 << 31) == EUNSUP
     assert call(lib, ws=None) == EWS
     assert call(lib, wsb=16) == EWS
