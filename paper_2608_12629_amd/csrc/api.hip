@@ -21,7 +21,8 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
     w.n_assign_blocks = (N + ppb - 1) / ppb;
   }
   w.n_sort_chunks = (N + RADIX_CHUNK - 1) / RADIX_CHUNK;
-  w.n_red_chunks = (N + RED_CR - 1) / RED_CR;
+  w.red_cr = red_slice(B, N);
+  w.n_red_chunks = (N + w.red_cr - 1) / w.red_cr;
   char* p = (char*)base;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -41,7 +42,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   w.keys_b = (int32_t*)take((size_t)(B * N) * 4);
   w.off = (int32_t*)take((size_t)(B * (K + 1)) * 4);
   w.perm = (int32_t*)take((size_t)(B * N) * 4);
-  w.carry = (float*)take((size_t)(B * w.n_red_chunks * 2 * D) * 4);
+  w.carry = (float*)take((size_t)(red_slices_bound(B, N) * 2 * D) * 4);
   w.sums = (float*)take((size_t)(B * K * D) * 4);
   const bool tiled = assign_tiled(dt, D);
   w.keys = (uint64_t*)take(tiled ? (size_t)(B * N) * 8 : 0);

@@ -210,14 +210,23 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
 // k-slice h (each lane group holds one contiguous half of the D dimensions)
 // and receives accumulator rows 8 q + 4 h + r (q, r = 0..3) of column n.
 // Each wave keeps NSUB 32-point column tiles in registers for the whole
-// kernel; centroids stream through LDS in stages of TCS = 2 tiles.
+// kernel; centroids stream through LDS in stages of TCS rows (four tiles, or
+// two for 512-byte rows, so that two stage buffers of two workgroups fit).
+//
+// Staging.  Each stage goes from L2 straight into LDS (global_load_lds, 16
+// bytes per lane, no registers, no LDS store instructions): lane l of a wave
+// fills LDS slot base + 16 l, so each lane fetches the centroid chunk that the
+// swizzled layout puts in its slot.  The two stage buffers are separate LDS
+// arrays: the compiler then sees that a load in flight into one buffer cannot
+// alias the reads of the other and does not wait for it before reading.
 //
 // Pipelining.  On this GPU the matrix pipe and the vector ALU overlap only
 // within one wave's instruction stream (a wave that only issues vector
 // instructions does not run beside another wave's MFMAs).  So the MFMAs of
 // tile t and the epilogue of tile t-1 are written into the same basic block,
 // on two accumulator sets, for the scheduler to interleave; NSUB independent
-// accumulation chains keep the matrix pipe fed.
+// accumulation chains keep the matrix pipe fed, and each MFMA is followed by
+// a few vector instructions and one LDS read of a later A operand.
 //
 // Epilogue.  The accumulator starts at -|c^|^2/2 - Q, with Q a bound on
 // |x|^2/2 over the workgroup's points plus a margin, so every score
@@ -230,26 +239,22 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
 // therefore count as ties and go to the lowest index; nothing else changes.
 // Padding rows score -FLT_MAX (an infinity with position bits would be a
 // signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
-template <int CPL, int LOADS>
-struct PipeStage {
-  u32x4 v[LOADS];  // native vectors: the struct stays in registers
-  float n;
-};
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
 
-// Per-lane LDS byte offsets, fixed for the whole kernel: where this thread
-// stores its stage chunks, and where it reads its A chunks and scores.
+// Per-lane offsets, fixed for the whole kernel.
 template <int CPL, int LOADS>
 struct PipeOffsets {
-  int store[LOADS];  // swizzled slot of chunk tid + u * 256 of a stage
-  int a[CPL];        // chunk h * CPL + c of centroid row n of tile 0
-  int n_store;       // score slot written by this thread
-  int n_read;        // first score read by this lane (rows 4 h .. 4 h + 3)
+  int src[LOADS];    // chunk of a stage that lands in LDS slot tid + u * 256
+  int a[CPL];        // byte offset of chunk h * CPL + c of centroid row n of tile 0
+  int n_store;       // byte offset of the score slot written by this thread
+  int n_read;        // byte offset of the first score read by this lane (rows 4 h .. 4 h + 3)
 };
 
-// Stage = two 32-centroid tiles: TCS rows of RC chunks, then TCS scores.
+// Stage = TCS centroid rows of RC 16-byte chunks (XOR-swizzled), then TCS scores.
 template <int CPL>
 struct PipeLayout {
-  static constexpr int TCS = ASSIGN_TCS, RC = 2 * CPL;
+  static constexpr int TCS = CPL <= 8 ? 128 : 64, RC = 2 * CPL, TILES = TCS / 32;
   static constexpr int SWZ = RC < 16 ? RC - 1 : 15;
   static constexpr int CHUNKS = TCS * RC * 16;          // bytes of centroid chunks
   static constexpr int STAGE = CHUNKS + TCS * 4;         // bytes per stage buffer
@@ -260,25 +265,15 @@ template <int CPL, int LOADS>
 __device__ __forceinline__ void pipe_offsets(PipeOffsets<CPL, LOADS>& o, int tid, int n, int h) {
   using L = PipeLayout<CPL>;
 #pragma unroll
-  for (int u = 0; u < LOADS; ++u) {
-    const int q = tid + u * ASSIGN_THREADS;
-    const int r = q / L::RC, c = q % L::RC;
-    o.store[u] = (r * L::RC + (c ^ (r & L::SWZ))) * 16;
+  for (int u = 0; u < LOADS; ++u) {  // slot s holds row s / RC, chunk (s % RC) ^ (row & SWZ)
+    const int sl = tid + u * ASSIGN_THREADS;
+    const int r = sl / L::RC;
+    o.src[u] = r * L::RC + ((sl % L::RC) ^ (r & L::SWZ));
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) o.a[c] = (n * L::RC + ((h * CPL + c) ^ (n & L::SWZ))) * 16;
   o.n_store = L::CHUNKS + (tid & (L::TCS - 1)) * 4;
   o.n_read = L::CHUNKS + 16 * h;
-}
-
-template <int CPL, int LOADS>
-__device__ __forceinline__ void pipe_load_stage(PipeStage<CPL, LOADS>& g, const u32x4* __restrict__ chat,
-                                                const float* __restrict__ cinit, int st, int tid) {
-  using L = PipeLayout<CPL>;
-  const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
-#pragma unroll
-  for (int u = 0; u < LOADS; ++u) g.v[u] = src[tid + u * ASSIGN_THREADS];
-  g.n = cinit[st * L::TCS + (tid & (L::TCS - 1))];
 }
 
 // LDS accesses at a per-lane offset plus a compile-time byte offset.
@@ -287,24 +282,32 @@ __device__ __forceinline__ T& lds_at(char* base, int lane_off, int imm) {
   return *reinterpret_cast<T*>(base + lane_off + imm);
 }
 
-template <int BUF, int CPL, int LOADS>
-__device__ __forceinline__ void pipe_store_stage(const PipeStage<CPL, LOADS>& g, char* lds,
-                                                 const PipeOffsets<CPL, LOADS>& o, float Q) {
+// Start stage `st` on its way into `buf` (complete after the wave's next
+// vmcnt(0) wait and a barrier) and fetch this thread's score for it.
+template <int CPL, int LOADS>
+__device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat,
+                                                  const float* __restrict__ cinit, int st, int tid,
+                                                  const PipeOffsets<CPL, LOADS>& o, char* buf) {
   using L = PipeLayout<CPL>;
+  const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
-  for (int u = 0; u < LOADS; ++u) lds_at<u32x4>(lds, o.store[u], BUF * L::STAGE) = g.v[u];
-  lds_at<float>(lds, o.n_store, BUF * L::STAGE) = g.n - Q;
+  for (int u = 0; u < LOADS; ++u)
+    __builtin_amdgcn_global_load_lds((global_void*)(src + o.src[u]),
+                                     (lds_void*)(buf + (u * ASSIGN_THREADS + wave * 64) * 16), 16, 0,
+                                     0);
+  return cinit[st * L::TCS + (tid & (L::TCS - 1))];
 }
 
 // The MFMAs of one 32-centroid tile into acc; each chain starts from the scores' init.
-template <int DT, int BUF, int TILE, int CPL, int NSUB, int LOADS>
+template <int DT, int TILE, int CPL, int NSUB, int LOADS>
 __device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 (&xr)[NSUB][CPL],
-                                               char* lds, const PipeOffsets<CPL, LOADS>& o) {
+                                               char* buf, const PipeOffsets<CPL, LOADS>& o) {
   using L = PipeLayout<CPL>;
   f32x16 cin;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const f32x4 v = lds_at<f32x4>(lds, o.n_read, BUF * L::STAGE + (TILE * 32 + 8 * q) * 4);
+    const f32x4 v = lds_at<f32x4>(buf, o.n_read, (TILE * 32 + 8 * q) * 4);
     cin[4 * q + 0] = v[0];
     cin[4 * q + 1] = v[1];
     cin[4 * q + 2] = v[2];
@@ -312,7 +315,7 @@ __device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    const uint4 a = lds_at<uint4>(lds, o.a[c], BUF * L::STAGE + TILE * L::TILE);
+    const uint4 a = lds_at<uint4>(buf, o.a[c], TILE * L::TILE);
 #pragma unroll
     for (int p = 0; p < NSUB; ++p) acc[p] = mfma32_chunk<DT>(a, xr[p][c], c == 0 ? cin : acc[p]);
   }
@@ -343,34 +346,44 @@ __device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_
   }
 }
 
-// One stage in buffer BUF: prefetch stage `next` from HBM/L2, run tile 0 on
-// accB beside the epilogue of the previous tile (accA), tile 1 on accA beside
-// the epilogue of tile 0, then store the prefetch into the other buffer.
-template <int DT, int BUF, int CPL, int NSUB, int LOADS>
+// One stage in `cur`: start the next stage into `nxt`, run the stage's tiles
+// (tile i on one accumulator set beside the epilogue of tile i-1 on the
+// other), store the next stage's scores, then wait for the loads and sync.
+template <int DT, int CPL, int NSUB, int LOADS>
 __device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
-                                           const uint4 (&xr)[NSUB][CPL], char* lds,
+                                           const uint4 (&xr)[NSUB][CPL], char* cur, char* nxt,
                                            const PipeOffsets<CPL, LOADS>& o, const u32x4* chat,
                                            const float* cinit, float Q, int tid,
                                            uint32_t& prev_code, float (&best)[NSUB],
                                            uint32_t (&code)[NSUB]) {
-  PipeStage<CPL, LOADS> pre;
-  pipe_load_stage<CPL, LOADS>(pre, chat, cinit, next, tid);
+  using L = PipeLayout<CPL>;
+  const float nn = pipe_issue_stage<CPL, LOADS>(chat, cinit, next, tid, o, nxt);
   // issue the prefetch first: left to the scheduler it drifts into the middle
-  // of the stage and the store at the end waits for it
+  // of the stage and the wait at the end stalls on it
   __builtin_amdgcn_sched_barrier(0);
-  const uint32_t code0 = (uint32_t)(2 * st) << 4, code1 = (uint32_t)(2 * st + 1) << 4;
-  pipe_mfma_tile<DT, BUF, 0, CPL, NSUB, LOADS>(accB, xr, lds, o);
+  const uint32_t tb = (uint32_t)(L::TILES * st);
+  pipe_mfma_tile<DT, 0, CPL, NSUB, LOADS>(accB, xr, cur, o);
   pipe_epilogue<NSUB>(accA, prev_code, best, code);
-  pipe_mfma_tile<DT, BUF, 1, CPL, NSUB, LOADS>(accA, xr, lds, o);
-  pipe_epilogue<NSUB>(accB, code0, best, code);
-  prev_code = code1;
-  pipe_store_stage<BUF ^ 1, CPL, LOADS>(pre, lds, o, Q);
-  // interleave: one MFMA, then a few vector instructions, repeated
+  pipe_mfma_tile<DT, 1, CPL, NSUB, LOADS>(accA, xr, cur, o);
+  pipe_epilogue<NSUB>(accB, tb << 4, best, code);
+  if constexpr (L::TILES == 4) {
+    pipe_mfma_tile<DT, 2, CPL, NSUB, LOADS>(accB, xr, cur, o);
+    pipe_epilogue<NSUB>(accA, (tb + 1) << 4, best, code);
+    pipe_mfma_tile<DT, 3, CPL, NSUB, LOADS>(accA, xr, cur, o);
+    pipe_epilogue<NSUB>(accB, (tb + 2) << 4, best, code);
+  }
+  prev_code = (tb + L::TILES - 1) << 4;
+  lds_at<float>(nxt, o.n_store, 0) = nn - Q;
+  // interleave: the first few LDS reads, then one MFMA, a few vector
+  // instructions and one LDS read, repeated
+  __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-  for (int i = 0; i < 2 * NSUB * CPL; ++i) {
+  for (int i = 0; i < L::TILES * NSUB * CPL; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 }
 
@@ -381,14 +394,15 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
     double* __restrict__ objpart) {
   static_assert(DT != DT_F32, "16-bit storage types only");
   using L = PipeLayout<CPL>;
-  static_assert(L::TCS == 64 && ASSIGN_KPAD % L::TCS == 0, "stage = two tiles, K padded to stages");
+  static_assert(ASSIGN_KPAD % L::TCS == 0, "K is padded to whole stages");
   constexpr int RC = L::RC;
   constexpr int PPW = 32 * NSUB;           // points per wave
   constexpr int PPB = 4 * PPW;             // points per workgroup
   constexpr int LOADS = L::TCS * RC / ASSIGN_THREADS;
   static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * RC, "stage must split evenly");
 
-  __shared__ __attribute__((aligned(16))) char lds[2 * L::STAGE];
+  __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
+  __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
   __shared__ float lds_q[4];
   __shared__ double lds_obj[4];
 
@@ -405,8 +419,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
 
   PipeOffsets<CPL, LOADS> o;
   pipe_offsets<CPL, LOADS>(o, tid, n, h);
-  PipeStage<CPL, LOADS> pre;
-  pipe_load_stage<CPL, LOADS>(pre, chat4, cinit, 0, tid);
+  const float n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
 
   const int pbase = blockIdx.x * PPB + wave * PPW;
   uint4 xr[NSUB][CPL];
@@ -451,18 +464,19 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
     for (int j = 0; j < 16; ++j) accA[p][j] = -0x1.fffffep127f;
   uint32_t prev_code = 0;
 
-  pipe_store_stage<0, CPL, LOADS>(pre, lds, o, Q);
+  lds_at<float>(buf0, o.n_store, 0) = n0 - Q;
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int st = 0;
-  for (; st + 2 <= nst; st += 2) {   // two stages per trip: buffer offsets are constants
-    pipe_stage<DT, 0, CPL, NSUB, LOADS>(st, st + 1, accA, accB, xr, lds, o, chat4, cinit, Q, tid,
-                                        prev_code, best, code);
-    pipe_stage<DT, 1, CPL, NSUB, LOADS>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr,
-                                        lds, o, chat4, cinit, Q, tid, prev_code, best, code);
+  for (; st + 2 <= nst; st += 2) {   // two stages per trip: each buffer is a fixed array
+    pipe_stage<DT, CPL, NSUB, LOADS>(st, st + 1, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q,
+                                     tid, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr, buf1,
+                                     buf0, o, chat4, cinit, Q, tid, prev_code, best, code);
   }
   if (st < nst)
-    pipe_stage<DT, 0, CPL, NSUB, LOADS>(st, st, accA, accB, xr, lds, o, chat4, cinit, Q, tid,
-                                        prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS>(st, st, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q, tid,
+                                     prev_code, best, code);
   pipe_epilogue<NSUB>(accA, prev_code, best, code);
 
   double obj = 0.0;

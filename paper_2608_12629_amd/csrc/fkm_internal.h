@@ -29,12 +29,27 @@ constexpr int ASSIGN_TCS = 64;
 constexpr int ASSIGN_KPAD = 128;
 inline int64_t kpad(int64_t K) { return (K + ASSIGN_KPAD - 1) / ASSIGN_KPAD * ASSIGN_KPAD; }
 // Update: the radix sort works on chunks of RADIX_CHUNK entries with digits of
-// at most RADIX_MAX_BITS bits; the segmented sum gives each wave RED_CR
-// consecutive entries of the sorted order.
+// at most RADIX_MAX_BITS bits; the segmented sum gives each wave a slice of
+// consecutive entries of the sorted order: the smallest power of two from
+// RED_MIN to RED_MAX that keeps the slice count at or below RED_WAVES, so that
+// small problems still spread over the whole chip.
 constexpr int RADIX_CHUNK = 4096;
 constexpr int RADIX_MAX_BITS = 8;
 constexpr int RADIX_MAX_R = 1 << RADIX_MAX_BITS;
-constexpr int RED_CR = 2048;
+constexpr int64_t RED_MIN = 128, RED_MAX = 2048, RED_WAVES = 4096;
+inline int64_t red_slice(int64_t B, int64_t N) {
+  int64_t r = RED_MIN;
+  while (r < RED_MAX && B * ((N + r - 1) / r) > RED_WAVES) r *= 2;
+  return r;
+}
+// An upper bound on B * ceil(N / red_slice(B, N)) that never decreases as N
+// grows, so a workspace sized for N also serves every smaller N.
+inline int64_t red_slices_bound(int64_t B, int64_t N) {
+  const int64_t fine = B * ((N + RED_MIN - 1) / RED_MIN);
+  const int64_t coarse = B * ((N + RED_MAX - 1) / RED_MAX);
+  const int64_t cap = coarse > RED_WAVES ? coarse : RED_WAVES;
+  return fine < cap ? fine : cap;
+}
 // Limits of this build.
 constexpr int64_t MAX_K = 65536;   // two radix passes of at most 8 bits
 constexpr int64_t MAX_D = 2048;
@@ -80,11 +95,11 @@ struct Workspace {
   int32_t* keys_b; // [B,N] cluster ids, sorted
   int32_t* off;    // [B,K+1] cluster start offsets in the sorted order
   int32_t* perm;   // [B,N] point ids sorted by cluster
-  float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by chunk ends
+  float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by slice ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
   uint64_t* keys;  // [B,N] best (score, index) of each point (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
-  int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks;
+  int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr;
   size_t total;
 };
 

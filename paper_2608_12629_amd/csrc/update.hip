@@ -6,7 +6,7 @@
 //   1. a stable radix sort of the point ids by cluster id (one or two passes of
 //      histogram, scan and LDS-staged scatter; see below)
 //   2. bounds     per cluster, its run [off_k, off_k+1) in the sorted order
-//   3. segreduce  one wave per RED_CR consecutive sorted entries streams the
+//   3. segreduce  one wave per slice of consecutive sorted entries streams the
 //                 whole rows X[perm[j]] and sums each cluster run in fp32 in a
 //                 fixed order; a run cut by a chunk end leaves a partial
 //   4. finalize   per cluster, the sum (or its partials, in chunk order) over
@@ -28,6 +28,32 @@ namespace fkm {
 namespace {
 
 __device__ __forceinline__ int digit_of(int key, int shift, int R) { return (key >> shift) & (R - 1); }
+
+static_assert(RADIX_MAX_R == 256, "the scans give each bin one thread of a 256-thread workgroup");
+
+// Exclusive scan of one value per thread over a 256-thread workgroup: a
+// shuffle scan inside each wave, then the four wave totals through `wsum`
+// (one barrier).  Returns the exclusive prefix; `total` gets the sum.
+__device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  int pre = 0;
+  total = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int s = wsum[i];
+    pre += i < w ? s : 0;
+    total += s;
+  }
+  return pre + x - v;
+}
 
 }  // namespace
 
@@ -60,7 +86,7 @@ __global__ __launch_bounds__(256) void radix_hist_kernel(const int32_t* __restri
 // of T, done by each scatter workgroup on its own (R <= 256 values).
 __global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H, int R, int nch,
                                                          int32_t* __restrict__ T) {
-  __shared__ int32_t part[256];
+  __shared__ int wsum[4];
   const int r = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   int32_t* h = H + ((size_t)b * R + r) * nch;
   const int per = (nch + 255) / 256;
@@ -73,15 +99,8 @@ __global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H
 #pragma unroll
     for (int u = 0; u < 16; ++u) sum += v[u];
   }
-  part[t] = sum;
-  __syncthreads();
-  for (int w = 1; w < 256; w <<= 1) {
-    const int a = t >= w ? part[t - w] : 0;
-    __syncthreads();
-    part[t] += a;
-    __syncthreads();
-  }
-  int run = part[t] - sum;
+  int bin_total;
+  int run = block_scan256(sum, wsum, bin_total);
   for (int c0 = i0; c0 < i1; c0 += 16) {
 #pragma unroll
     for (int u = 0; u < 16; ++u) v[u] = c0 + u < i1 ? h[c0 + u] : 0;
@@ -91,19 +110,21 @@ __global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H
       run += v[u];
     }
   }
-  if (t == 255) T[(size_t)b * RADIX_MAX_R + r] = part[255];
+  if (t == 0) T[(size_t)b * RADIX_MAX_R + r] = bin_total;
 }
 
+template <int DBITS>
 __global__ __launch_bounds__(256) void radix_scatter_kernel(
     const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int N, int K,
-    const int32_t* __restrict__ total, int shift, int dbits, int nch,
+    const int32_t* __restrict__ total, int shift, int nch,
     const int32_t* __restrict__ H, const int32_t* __restrict__ T, int32_t* __restrict__ total_out,
     int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
   constexpr int STEPS = RADIX_CHUNK / 256;  // 64-entry steps per wave
   __shared__ int skey[RADIX_CHUNK], sval[RADIX_CHUNK];
   __shared__ int cur[4][RADIX_MAX_R];
-  __shared__ int lstart[RADIX_MAX_R + 1], gstart[RADIX_MAX_R], bstart[RADIX_MAX_R + 1];
-  const int R = 1 << dbits;
+  __shared__ int lstart[RADIX_MAX_R], gstart[RADIX_MAX_R];
+  __shared__ int wsum[2][4];
+  constexpr int R = 1 << DBITS;
   const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int n_in = total ? total[b] : N;
@@ -119,50 +140,37 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
     k[s] = in ? kb[i] : -1;
     v[s] = in ? (vb ? vb[i] : i) : 0;
   }
-  for (int r = t; r < 4 * RADIX_MAX_R; r += 256) (&cur[0][0])[r] = 0;
-  // bin starts: exclusive scan of the bin totals
-  if (t < RADIX_MAX_R) bstart[t + 1] = t < R ? T[(size_t)b * RADIX_MAX_R + t] : 0;
-  if (t == 0) bstart[0] = 0;
-  __syncthreads();
-  for (int d = 1; d <= RADIX_MAX_R; d <<= 1) {
-    int add = 0;
-    if (t < RADIX_MAX_R && t + 1 > d) add = bstart[t + 1 - d];
-    __syncthreads();
-    if (t < RADIX_MAX_R) bstart[t + 1] += add;
-    __syncthreads();
-  }
-  if (total_out && ch == 0 && t == 0) total_out[b] = bstart[RADIX_MAX_R];
+  // this bin's total over all chunks and its count before this chunk
+  const int tbin = t < R ? T[(size_t)b * RADIX_MAX_R + t] : 0;
+  const int hrun = t < R ? H[((size_t)b * R + t) * nch + ch] : 0;
+#pragma unroll
+  for (int ww = 0; ww < 4; ++ww) cur[ww][t] = 0;  // RADIX_MAX_R == 256 == blockDim
+  // bin starts: exclusive scan of the bin totals (its barrier also orders the zeroing)
+  int n_valid;
+  const int bstart = block_scan256(tbin, wsum[0], n_valid);
+  if (total_out && ch == 0 && t == 0) total_out[b] = n_valid;
   // per-wave bin counts (integer atomics: exact)
 #pragma unroll
   for (int s = 0; s < STEPS; ++s)
     if ((unsigned)k[s] < (unsigned)K) atomicAdd(&cur[w][digit_of(k[s], shift, R)], 1);
   __syncthreads();
-  // chunk totals per bin -> exclusive scan over bins (lstart); wave starts per bin
-  if (t < RADIX_MAX_R) {
-    int tot = 0;
-    if (t < R) {
+  // this chunk's count per bin -> exclusive scan over bins; wave starts per bin
+  int c4[4], tot = 0;
 #pragma unroll
-      for (int ww = 0; ww < 4; ++ww) tot += cur[ww][t];
-      gstart[t] = bstart[t] + H[((size_t)b * R + t) * nch + ch];
-    }
-    lstart[t + 1] = tot;
+  for (int ww = 0; ww < 4; ++ww) {
+    c4[ww] = t < R ? cur[ww][t] : 0;
+    tot += c4[ww];
   }
-  if (t == 0) lstart[0] = 0;
-  __syncthreads();
-  for (int d = 1; d <= RADIX_MAX_R; d <<= 1) {  // inclusive scan of lstart[1..R]
-    int add = 0;
-    if (t < RADIX_MAX_R && t + 1 > d) add = lstart[t + 1 - d];
-    __syncthreads();
-    if (t < RADIX_MAX_R) lstart[t + 1] += add;
-    __syncthreads();
-  }
+  int nloc;
+  const int ls = block_scan256(tot, wsum[1], nloc);
   if (t < R) {
-    int run = lstart[t];
+    lstart[t] = ls;
+    gstart[t] = bstart + hrun;
+    int run = ls;
 #pragma unroll
     for (int ww = 0; ww < 4; ++ww) {
-      const int c = cur[ww][t];
       cur[ww][t] = run;
-      run += c;
+      run += c4[ww];
     }
   }
   __syncthreads();
@@ -172,11 +180,15 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   for (int s = 0; s < STEPS; ++s) {
     const bool valid = (unsigned)k[s] < (unsigned)K;
     const int dg = valid ? digit_of(k[s], shift, R) : 0;
+    // lanes holding the same digit: for each bit keep the lanes that agree
+    // (invalid lanes hold digit 0 and are dropped by the first ballot)
     uint64_t match = __ballot(valid);
-    for (int bit = 0; bit < dbits; ++bit) {
-      const bool on = (dg >> bit) & 1;
-      const uint64_t bb = __ballot(valid && on);
-      match &= on ? bb : ~bb;
+#pragma unroll
+    for (int bit = 0; bit < DBITS; ++bit) {
+      const int on = (dg >> bit) & 1;
+      const uint64_t bb = __ballot(on);
+      const uint64_t flip = (uint64_t)(int64_t)(on - 1);  // all ones where the bit is clear
+      match &= bb ^ flip;
     }
     if (valid) {
       const int rank = __popcll(match & below);
@@ -188,15 +200,18 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   }
   __syncthreads();
   // write each bin's run contiguously
-  const int nloc = lstart[R];
   int32_t* ko = keys_out ? keys_out + (size_t)b * N : nullptr;
   int32_t* vo = vals_out + (size_t)b * N;
-  for (int j = t; j < nloc; j += 256) {
-    const int key = skey[j];
-    const int dg = digit_of(key, shift, R);
-    const int g = gstart[dg] + (j - lstart[dg]);
-    if (ko) ko[g] = key;
-    vo[g] = sval[j];
+#pragma unroll 4
+  for (int s = 0; s < STEPS; ++s) {
+    const int j = s * 256 + t;
+    if (j < nloc) {
+      const int key = skey[j];
+      const int dg = digit_of(key, shift, R);
+      const int g = gstart[dg] + (j - lstart[dg]);
+      if (ko) ko[g] = key;
+      vo[g] = sval[j];
+    }
   }
 }
 
@@ -262,7 +277,7 @@ template <> struct Row<DT_F16> {
 template <int DT, int LPR, int CPLR>
 __global__ __launch_bounds__(256) void segreduce_kernel(
     const uint4* __restrict__ X, const int32_t* __restrict__ perm, const int32_t* __restrict__ off,
-    int N, int K, int nred, float* __restrict__ sums, float* __restrict__ carry) {
+    int N, int K, int nred, int cr, float* __restrict__ sums, float* __restrict__ carry) {
   constexpr int E = Row<DT>::per16;
   constexpr int RC = LPR * CPLR;
   constexpr int D = RC * E;
@@ -274,8 +289,8 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
   const int b = blockIdx.y;
   if (w >= nred) return;
   const int32_t* ob = off + (size_t)b * (K + 1);
-  const int j0 = w * RED_CR;
-  const int j1 = min(ob[K], j0 + RED_CR);  // ob[K] = number of sorted (valid) entries
+  const int j0 = w * cr;
+  const int j1 = min(ob[K], j0 + cr);  // ob[K] = number of sorted (valid) entries
   if (j0 >= j1) return;
   const int32_t* pb = perm + (size_t)b * N;
   const uint4* xb = X + (size_t)b * N * RC;
@@ -355,7 +370,7 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
 __global__ __launch_bounds__(256) void finalize_kernel(
     const float* __restrict__ sums, const float* __restrict__ carry,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ off,
-    const float* C_prev, int K, int D, int nred, float* C_out) {
+    const float* C_prev, int K, int D, int nred, int cr, float* C_out) {
   extern __shared__ float4 part[];
   const int k = blockIdx.x, b = blockIdx.y;
   const int t = threadIdx.x;
@@ -369,7 +384,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     return;
   }
   const int j0 = off[(size_t)b * (K + 1) + k], j1 = off[(size_t)b * (K + 1) + k + 1];
-  const int c0 = j0 / RED_CR, c1 = (j1 - 1) / RED_CR;
+  const int c0 = j0 / cr, c1 = (j1 - 1) / cr;
   const float fn = (float)n;
   if (c0 == c1) {
     for (int d = t; d < D4; d += 256) {
@@ -385,7 +400,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (slot < slots && d < D4) {
       for (int c = c0 + slot; c <= c1; c += slots) {
-        const int which = (c == c0 && j0 > c * RED_CR) ? 1 : 0;
+        const int which = (c == c0 && j0 > c * cr) ? 1 : 0;
         const float4 v = reinterpret_cast<const float4*>(
             carry + (((size_t)b * nred + c) * 2 + which) * D)[d];
         s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
@@ -411,8 +426,8 @@ static void launch_segreduce(const void* X, const Workspace& w, int64_t B, int64
                              hipStream_t s) {
   const dim3 grid((unsigned)((w.n_red_chunks + 3) / 4), (unsigned)B), block(256);
   segreduce_kernel<DT, LPR, CPLR><<<grid, block, 0, s>>>((const uint4*)X, w.perm, w.off, (int)N,
-                                                         (int)K, (int)w.n_red_chunks, w.sums,
-                                                         w.carry);
+                                                         (int)K, (int)w.n_red_chunks,
+                                                         (int)w.red_cr, w.sums, w.carry);
 }
 
 template <int DT>
@@ -441,6 +456,22 @@ static hipError_t launch_segreduce_dt(const void* X, const Workspace& w, int64_t
 
 hipError_t update_init() { return hipSuccess; }
 
+template <typename... A>
+static hipError_t launch_scatter(int dbits, dim3 grid, hipStream_t s, A... a) {
+  switch (dbits) {
+    case 1: radix_scatter_kernel<1><<<grid, 256, 0, s>>>(a...); break;
+    case 2: radix_scatter_kernel<2><<<grid, 256, 0, s>>>(a...); break;
+    case 3: radix_scatter_kernel<3><<<grid, 256, 0, s>>>(a...); break;
+    case 4: radix_scatter_kernel<4><<<grid, 256, 0, s>>>(a...); break;
+    case 5: radix_scatter_kernel<5><<<grid, 256, 0, s>>>(a...); break;
+    case 6: radix_scatter_kernel<6><<<grid, 256, 0, s>>>(a...); break;
+    case 7: radix_scatter_kernel<7><<<grid, 256, 0, s>>>(a...); break;
+    case 8: radix_scatter_kernel<8><<<grid, 256, 0, s>>>(a...); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 // Digit widths: the key needs `bits` bits; one pass for <= 8 bits, else two
 // passes of about half each.
 static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
@@ -467,10 +498,10 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
     if ((e = hipGetLastError()) != hipSuccess) return e;
     radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    radix_scatter_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(
-        idx, nullptr, (int)N, (int)K, nullptr, 0, d1, nch, w.rhist, w.rbin, w.rtotal,
-        passes == 1 ? w.keys_b : w.keys_a, passes == 1 ? w.perm : w.vals_a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scatter(d1, dim3(nch, (unsigned)B), s, idx, nullptr, (int)N, (int)K, nullptr, 0,
+                            nch, w.rhist, w.rbin, w.rtotal, passes == 1 ? w.keys_b : w.keys_a,
+                            passes == 1 ? w.perm : w.vals_a)) != hipSuccess)
+      return e;
   }
   if (passes == 2) {
     const int R = 1 << d2;
@@ -479,10 +510,10 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
     if ((e = hipGetLastError()) != hipSuccess) return e;
     radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    radix_scatter_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(
-        w.keys_a, w.vals_a, (int)N, (int)K, w.rtotal, d1, d2, nch, w.rhist, w.rbin, nullptr,
-        w.keys_b, w.perm);  // the second pass keeps the same total
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scatter(d2, dim3(nch, (unsigned)B), s, w.keys_a, w.vals_a, (int)N, (int)K,
+                            w.rtotal, d1, nch, w.rhist, w.rbin, nullptr, w.keys_b,
+                            w.perm)) != hipSuccess)  // the second pass keeps the same total
+      return e;
   }
   bounds_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
       w.keys_b, w.rtotal, (int)N, (int)K, w.off, counts);
@@ -493,7 +524,8 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
   if (e != hipSuccess) return e;
   const size_t part_bytes = 256 * sizeof(float4);
   finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, part_bytes, s>>>(
-      w.sums, w.carry, counts, w.off, C_prev, (int)K, (int)D, (int)w.n_red_chunks, C_out);
+      w.sums, w.carry, counts, w.off, C_prev, (int)K, (int)D, (int)w.n_red_chunks, (int)w.red_cr,
+      C_out);
   return hipGetLastError();
 }
 
