@@ -30,7 +30,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
     o = align_up(o + bytes);
     return r;
   };
-  w.Kp = kpad(K);
+  w.Kp = kpad_for(dt, D, K);
   w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
   w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
   w.objpart = (double*)take((size_t)(B * w.n_assign_blocks) * 8);

@@ -1,32 +1,74 @@
 // assign_tiled.hip -- the assignment step for wide rows (16-bit points with
 // D >= 512), where a point no longer fits in registers.
 //
-// The distance contraction is tiled like a GEMM: a workgroup owns 256 points
-// (4 waves x 64) and TILED_CBG consecutive 128-centroid blocks; for each block
-// it streams D in 32-dimension stages through LDS (points and centroids, both
-// double-buffered) and runs 32x32x16 MFMAs, 8 independent accumulators per
-// wave (2 point tiles x 4 centroid tiles).  After each block an exact
-// compare-and-select keeps each lane's best (score, index); after the group
-// the workgroup merges its result into a per-point 64-bit key with atomicMax.
-// The key is the score mapped to an order-preserving unsigned integer in the
-// high half and the complemented index in the low half, so the maximum is the
-// largest score and, among equal scores, the lowest index: the same result
-// as a sequential scan, whatever order the workgroups finish in.
+// The distance contraction is tiled like a GEMM.  A workgroup owns 256 points
+// and up to TILED_CBG consecutive 256-centroid blocks; its four waves split
+// each 256 x 256 block 2 x 2, so a wave owns 128 points x 128 centroids: 4 x 4
+// 32x32x16 MFMA tiles, 16 independent accumulators (one wave per SIMD).  Per
+// 16-dimension step a wave reads 4 centroid and 4 point fragments from LDS
+// for 16 MFMAs.
 //
-// Block order is XCD-aware: consecutive workgroup ids go to different XCDs,
-// so the ids are remapped for each XCD to own whole point blocks (all their
-// centroid groups run on one XCD and find the point block in that XCD's L2).
+// Staging.  D streams through LDS in 32-dimension stages holding both
+// operands and the block's scores.  Each stage goes from L2 straight into LDS
+// (global_load_lds: lane l of a wave fills slot base + 16 l, so each lane
+// fetches the chunk the swizzled layout puts there).  Four stage buffers let
+// the loads run two to three stages ahead: a barrier without a memory fence
+// (an explicit vmcnt wait for exactly the stage needed next, then s_barrier)
+// keeps the later stages in flight across it.  The buffers are separate LDS
+// arrays and the stage loop is unrolled by four, so the compiler sees that
+// loads in flight into other buffers never alias a stage's reads.  The
+// barrier sits in the middle of a stage: the second 16-dimension step's
+// MFMAs run after it, beside the reads of the next stage's first fragments.
+//
+// Scores.  As in the resident kernel, the accumulator starts at
+// -|c^|^2/2 - Q, with Q a bound on |x|^2/2 over the workgroup's 256 points
+// (from a row-norm pass) plus a margin, so every score is negative and the
+// packed-key epilogue applies: the lane's position j in the tile goes into the
+// 4 low mantissa bits, a max3 tree picks the tile's best, and a strict compare
+// on the masked value keeps the earliest tile (scores within 16 ulp count as
+// ties and go to the lowest index).  The two waves sharing a point range merge
+// through LDS at the end, and the workgroup merges its result into a
+// per-point 64-bit key with atomicMax: the masked score mapped to an
+// order-preserving unsigned integer in the high half and the complemented
+// index in the low half, so the maximum is the largest score and, among equal
+// scores, the lowest index, whatever order the workgroups finish in.  Q
+// depends only on the point block, so every workgroup of a point block uses
+// the same Q, and the decode pass recomputes it the same way.
+//
+// Block order is XCD-aware: workgroup ids go round-robin over the 8 XCDs, and
+// each XCD walks super-tiles of 8 point blocks x all centroid groups (point
+// block fastest), so the workgroups resident on an XCD share both operands
+// through that XCD's L2.
 #include "fkm_device.h"
 
 namespace fkm {
 
 namespace {
 
-constexpr int BP = 256;           // points per workgroup
-constexpr int BC = TILED_BC;      // centroids per block
-constexpr int DC = 32;            // dimensions per LDS stage
-constexpr int CPS = DC * 2 / 16;  // 16-byte chunks of a row in one stage (4)
-static_assert(BC == 128, "four 32-row tiles per centroid block");
+constexpr int BP = TILED_BP;             // points per workgroup
+constexpr int BC = TILED_BC;             // centroids per block
+constexpr int DC = 32;                   // dimensions per LDS stage
+constexpr int CPS = DC * 2 / 16;         // 16-byte chunks of a row in one stage (4)
+constexpr int XB = BP * CPS * 16;        // bytes of point chunks per stage
+constexpr int CB = BC * CPS * 16;        // bytes of centroid chunks per stage
+constexpr int STAGE = XB + CB + BC * 4;  // + the block's scores
+constexpr int LX = BP * CPS / 256;       // point chunks per thread per stage
+constexpr int LC = BC * CPS / 256;       // centroid chunks per thread per stage
+constexpr int LOADS = LX + LC + 1;       // loads per thread per stage (+ one score)
+static_assert(BP == 256 && BC == 256, "2 x 2 waves of 128 x 128");
+static_assert(2 * LOADS <= 63, "vmcnt counts at most 63 loads");
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wait until at most n of this wave's loads are in flight and its LDS
+// accesses are done, then a barrier without a memory fence, so the loads
+// started into other buffers stay in flight across it.
+template <int n>
+__device__ __forceinline__ void wait_loads_and_sync() {
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (7 << 4));
+  asm volatile("s_barrier" ::: "memory");
+}
 
 // Row r of a stage keeps its 4 chunks in slots c ^ f(r); f spreads 16
 // consecutive rows over distinct banks for 16-byte reads.
@@ -40,168 +82,289 @@ __device__ __forceinline__ float unordered(uint32_t u) {
   return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
 }
 
-struct TiledStage {
-  u32x4 x[4], c[2];  // native vectors: the stage stays in registers
-  float n;
-};
-
-__device__ __forceinline__ void tiled_load(TiledStage& g, const uint4* __restrict__ X,
-                                           const uint4* __restrict__ chat,
-                                           const float* __restrict__ cinit, int s, int nds, int p0,
-                                           int cb0, int N, int RC, int tid) {
-  const int gb = s / nds, ds = s % nds;
-  const u32x4* x4 = reinterpret_cast<const u32x4*>(X);
-  const u32x4* c4 = reinterpret_cast<const u32x4*>(chat);
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int q = tid + u * 256, r = q >> 2, c = q & 3;
-    g.x[u] = p0 + r < N ? x4[(size_t)(p0 + r) * RC + ds * CPS + c] : u32x4{0u, 0u, 0u, 0u};
-  }
-  const int crow = (cb0 + gb) * BC;
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int q = tid + u * 256, r = q >> 2, c = q & 3;
-    g.c[u] = c4[(size_t)(crow + r) * RC + ds * CPS + c];
-  }
-  g.n = cinit[crow + (tid & (BC - 1))];
+// Q >= max |x|^2 / 2 over a point block, with a relative margin of 2^-8; the
+// same bits wherever it is computed from the same norms.
+__device__ __forceinline__ float block_q(float xmax) {
+  return __builtin_fmaf(0.5f * xmax, 1.0f + 0x1p-8f, 1e-30f);
 }
 
-__device__ __forceinline__ void tiled_store(const TiledStage& g, uint4* lx, uint4* lc, float* ln,
-                                            int tid) {
+template <typename T>
+__device__ __forceinline__ T& lds_at(char* base, int off) {
+  return *reinterpret_cast<T*>(base + off);
+}
+
+struct TiledCtx {
+  const char* X;       // the workgroup's first point row
+  const char* chat;    // this instance's rounded centroids
+  const float* cinit;  // this instance's -|c^|^2/2
+  uint32_t xoff;       // lane byte offset of its first point chunk (row clamped to the last point)
+  uint32_t coff;       // lane byte offset of its first centroid chunk
+  uint32_t rows64;     // bytes of 64 rows
+  int last;            // last valid row of the point block
+  int nds, cb0, RC, tid, S, loff0, loff1, wp, wc;
+};
+
+// Stage s = (block s / nds, dimensions 32 (s % nds) ..): start its loads into buf.
+// Load u of a thread covers slot tid + 256 u: row tid / 4 + 64 u, chunk
+// (tid % 4) ^ swz(row) (swz has period 16, so the chunk order repeats).
+__device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf) {
+  const int g = s / c.nds, ds = s % c.nds;
+  const int wave = __builtin_amdgcn_readfirstlane(c.tid >> 6);
+  const char* xb = c.X + ds * CPS * 16;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int q = tid + u * 256, r = q >> 2, c = q & 3;
-    reinterpret_cast<u32x4*>(lx)[r * CPS + (c ^ swz(r))] = g.x[u];
+  for (int u = 0; u < LX; ++u) {
+    // rows past the last point reload the last point (their results are dropped)
+    const uint32_t off = (c.tid >> 2) + 64 * u <= c.last
+                             ? c.xoff + u * c.rows64
+                             : (uint32_t)((c.last * c.RC + ((c.tid & 3) ^ swz(c.tid >> 2))) * 16);
+    __builtin_amdgcn_global_load_lds((global_void*)(xb + off),
+                                     (lds_void*)(buf + (u * 256 + wave * 64) * 16), 16, 0, 0);
   }
+  const int krow = (c.cb0 + g) * BC;
+  const char* cbp = c.chat + ((size_t)krow * c.RC + ds * CPS) * 16;
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int q = tid + u * 256, r = q >> 2, c = q & 3;
-    reinterpret_cast<u32x4*>(lc)[r * CPS + (c ^ swz(r))] = g.c[u];
+  for (int u = 0; u < LC; ++u)
+    __builtin_amdgcn_global_load_lds((global_void*)(cbp + c.coff + u * c.rows64),
+                                     (lds_void*)(buf + XB + (u * 256 + wave * 64) * 16), 16, 0, 0);
+  // the block's scores ride with every stage, so every stage issues LOADS loads
+  __builtin_amdgcn_global_load_lds((global_void*)(c.cinit + krow + c.tid),
+                                   (lds_void*)(buf + XB + CB + wave * 256), 4, 0, 0);
+}
+
+// Fragments of one 16-dimension step: 4 centroid tiles and 4 point tiles.
+struct TiledFrag {
+  uint4 a[4], b[4];
+};
+
+__device__ __forceinline__ void tiled_read(TiledFrag& f, char* buf, int lo, int wp, int wc) {
+#pragma unroll
+  for (int tc = 0; tc < 4; ++tc) f.a[tc] = lds_at<uint4>(buf, XB + (wc * 128 + tc * 32) * 64 + lo);
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp) f.b[tp] = lds_at<uint4>(buf, (wp * 128 + tp * 32) * 64 + lo);
+}
+
+template <int DT>
+__device__ __forceinline__ void tiled_mfma(f32x16 (&acc)[4][4], const TiledFrag& f) {
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp)
+#pragma unroll
+    for (int tc = 0; tc < 4; ++tc) acc[tp][tc] = mfma32_chunk<DT>(f.a[tc], f.b[tp], acc[tp][tc]);
+}
+
+// A new block: every accumulator starts at its centroid's -|c^|^2/2 - Q.
+__device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][4], char* buf, int wc, int h, float Q) {
+#pragma unroll
+  for (int tc = 0; tc < 4; ++tc) {
+    f32x16 cin;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 v = lds_at<f32x4>(buf, XB + CB + (wc * 128 + tc * 32 + 8 * q + 4 * h) * 4);
+      cin[4 * q + 0] = v[0] - Q;
+      cin[4 * q + 1] = v[1] - Q;
+      cin[4 * q + 2] = v[2] - Q;
+      cin[4 * q + 3] = v[3] - Q;
+    }
+#pragma unroll
+    for (int tp = 0; tp < 4; ++tp) acc[tp][tc] = cin;
   }
-  ln[tid & (BC - 1)] = g.n;
+}
+
+// Stage s in `cur` (its first-step fragments already in f0): read the second
+// step's, run the first step's MFMAs, wait for stage s + 1 and sync, start
+// stage s + 3 into `ahead` (the buffer of stage s - 1, which every wave has
+// now finished), read stage s + 1's first-step fragments from `nxt`, run the
+// second step's MFMAs.  TAIL: stages past the end may follow.
+template <int DT, bool TAIL>
+__device__ __forceinline__ void tiled_stage(const TiledCtx& c, int s, char* cur, char* nxt,
+                                            char* ahead, f32x16 (&acc)[4][4], TiledFrag& f0,
+                                            TiledFrag& f1) {
+  tiled_read(f1, cur, c.loff1, c.wp, c.wc);
+  tiled_mfma<DT>(acc, f0);
+  if (!TAIL || s + 2 < c.S) wait_loads_and_sync<LOADS>();
+  else wait_loads_and_sync<0>();
+  if (!TAIL || s + 3 < c.S) tiled_issue(c, s + 3, ahead);
+  if (!TAIL || s + 1 < c.S) tiled_read(f0, nxt, c.loff0, c.wp, c.wc);
+  tiled_mfma<DT>(acc, f1);
+}
+
+// Four stages; stage s0 is in buffer 0.
+template <int DT, bool TAIL>
+__device__ __forceinline__ void tiled_quad(const TiledCtx& c, int s0, char* b0, char* b1, char* b2,
+                                           char* b3, f32x16 (&acc)[4][4], TiledFrag& f0,
+                                           TiledFrag& f1) {
+  tiled_stage<DT, TAIL>(c, s0, b0, b1, b3, acc, f0, f1);
+  tiled_stage<DT, TAIL>(c, s0 + 1, b1, b2, b0, acc, f0, f1);
+  tiled_stage<DT, TAIL>(c, s0 + 2, b2, b3, b1, acc, f0, f1);
+  tiled_stage<DT, TAIL>(c, s0 + 3, b3, b0, b2, acc, f0, f1);
+}
+
+// The block is complete: packed-key arg-max of each tile into the running
+// (best, code) of each point tile; tiles are visited in increasing index order.
+__device__ __forceinline__ void tiled_epilogue(const f32x16 (&acc)[4][4], float (&best)[4],
+                                               uint32_t (&code)[4], uint32_t tile0) {
+#pragma unroll
+  for (int tp = 0; tp < 4; ++tp)
+#pragma unroll
+    for (int tc = 0; tc < 4; ++tc) {
+      float k[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        k[j] = __uint_as_float((__float_as_uint(acc[tp][tc][j]) & ~15u) | (uint32_t)j);
+      const float t0 = __builtin_fmaxf(__builtin_fmaxf(k[0], k[1]), k[2]);
+      const float t1 = __builtin_fmaxf(__builtin_fmaxf(k[3], k[4]), k[5]);
+      const float t2 = __builtin_fmaxf(__builtin_fmaxf(k[6], k[7]), k[8]);
+      const float t3 = __builtin_fmaxf(__builtin_fmaxf(k[9], k[10]), k[11]);
+      const float t4 = __builtin_fmaxf(__builtin_fmaxf(k[12], k[13]), k[14]);
+      const float u0 = __builtin_fmaxf(__builtin_fmaxf(t0, t1), t2);
+      const float u1 = __builtin_fmaxf(__builtin_fmaxf(t3, t4), k[15]);
+      const uint32_t mb = __float_as_uint(__builtin_fmaxf(u0, u1));
+      const float mm = __uint_as_float(mb & ~15u);
+      const bool gt = mm > best[tp];
+      best[tp] = gt ? mm : best[tp];
+      code[tp] = gt ? ((mb & 15u) | ((tile0 + tc) << 4)) : code[tp];
+    }
 }
 
 }  // namespace
 
 template <int DT>
-__global__ __launch_bounds__(256, 2) void assign_tiled_kernel(
+__global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
-    int N, int D, int Kp, int npb, int ncbg, uint64_t* __restrict__ keys,
-    float* __restrict__ xnorm) {
-  __shared__ uint4 lx[2][BP * CPS];                              // 2 x 16 KiB
-  __shared__ uint4 lc[2][BC * CPS];                              // 2 x 8 KiB
-  __shared__ __attribute__((aligned(16))) float ln[2][BC];
+    const float* __restrict__ xnorm, int N, int D, int Kp, int npb, int ncbg,
+    uint64_t* __restrict__ keys) {
+  __shared__ __attribute__((aligned(16))) char buf0[STAGE];
+  __shared__ __attribute__((aligned(16))) char buf1[STAGE];
+  __shared__ __attribute__((aligned(16))) char buf2[STAGE];
+  __shared__ __attribute__((aligned(16))) char buf3[STAGE];
+  __shared__ float lds_q[4];
 
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
-  // XCD-aware remap: XCD x (= id % 8) takes point blocks x, x + 8, ... in turn,
-  // each with all of its centroid groups
+  const int wp = wave & 1, wc = wave >> 1;
   const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int pb = xcd + 8 * (j / ncbg), cbg = j % ncbg;
+  const int sup = j / (8 * ncbg), cbg = (j / 8) % ncbg;
+  const int pb = (sup * 8 + xcd) * 8 + (j & 7);
   if (pb >= npb) return;
-  const int ncb = Kp / BC;
-  const int cb0 = cbg * TILED_CBG;
-  const int ncbw = min(TILED_CBG, ncb - cb0);  // centroid blocks of this workgroup
-  const int RC = D / 8;                         // 16-byte chunks per row
-  const int nds = D / DC;                       // stages per centroid block
-  const int S = ncbw * nds;
-  X += (size_t)b * N * RC;
-  chat += (size_t)b * Kp * RC;
-  cinit += (size_t)b * Kp;
   const int p0 = pb * BP;
-  const bool do_norm = cbg == 0;
+  const int RC = D / 8;  // 16-byte chunks per row
+  const int nds = D / DC;
+  const int cb0 = cbg * TILED_CBG;
+  const int ncbw = min(TILED_CBG, Kp / BC - cb0);  // centroid blocks of this workgroup
 
-  // stage s: centroid block cb0 + s / nds, dimensions [32 (s % nds), +32)
-  TiledStage pre;
-  f32x16 acc[2][4];
-  float best[2] = {-__builtin_inff(), -__builtin_inff()};
-  int bidx[2] = {0, 0};
-  float xs = 0.f;  // squared norm of point p0 + tid (first group only)
+  TiledCtx c;
+  c.X = reinterpret_cast<const char*>(X + ((size_t)b * N + p0) * RC);
+  c.chat = reinterpret_cast<const char*>(chat + (size_t)b * Kp * RC);
+  c.cinit = cinit + (size_t)b * Kp;
+  c.last = min(BP, N - p0) - 1;
+  c.xoff = (uint32_t)((min(tid >> 2, c.last) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
+  c.coff = (uint32_t)(((tid >> 2) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
+  c.rows64 = (uint32_t)(64 * RC * 16);
+  c.nds = nds;
+  c.cb0 = cb0;
+  c.RC = RC;
+  c.tid = tid;
+  c.S = ncbw * nds;
+  // fragment reads: lane 32 h + n takes row (tile base + n), chunk 2 ks + h
+  c.loff0 = n * 64 + ((0 + h) ^ swz(n)) * 16;
+  c.loff1 = n * 64 + ((2 + h) ^ swz(n)) * 16;
+  c.wp = wp;
+  c.wc = wc;
 
-  tiled_load(pre, X, chat, cinit, 0, nds, p0, cb0, N, RC, tid);
-  tiled_store(pre, lx[0], lc[0], ln[0], tid);
-  __syncthreads();
-  for (int s = 0; s < S; ++s) {
-    const int buf = s & 1;
-    const int g = s / nds, ds = s % nds;
-    if (s + 1 < S) tiled_load(pre, X, chat, cinit, s + 1, nds, p0, cb0, N, RC, tid);
-    if (ds == 0) {
+  // Q of the point block
+  float xm = tid <= c.last ? xnorm[(size_t)b * N + p0 + tid] : 0.f;
 #pragma unroll
-      for (int tc = 0; tc < 4; ++tc) {
-        f32x16 cin;
+  for (int m = 1; m < 64; m <<= 1) xm = __builtin_fmaxf(xm, __shfl_xor(xm, m));
+  if (lane == 0) lds_q[wave] = xm;
+
+  // stages 0 .. 2 in flight before the loop; stage 0 complete
+  const int S = c.S;
+  tiled_issue(c, 0, buf0);
+  if (1 < S) tiled_issue(c, 1, buf1);
+  if (2 < S) tiled_issue(c, 2, buf2);
+  if (2 < S) wait_loads_and_sync<2 * LOADS>();
+  else if (1 < S) wait_loads_and_sync<LOADS>();
+  else wait_loads_and_sync<0>();
+  const float Q =
+      block_q(__builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])));
+
+  f32x16 acc[4][4];
+  float best[4];
+  uint32_t code[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x4 v = *reinterpret_cast<const f32x4*>(&ln[buf][tc * 32 + 8 * q + 4 * h]);
-          cin[4 * q + 0] = v[0];
-          cin[4 * q + 1] = v[1];
-          cin[4 * q + 2] = v[2];
-          cin[4 * q + 3] = v[3];
-        }
-        acc[0][tc] = cin;
-        acc[1][tc] = cin;
-      }
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int c = 2 * ks + h;
-      uint4 a[4], bx[2];
-#pragma unroll
-      for (int tc = 0; tc < 4; ++tc) {
-        const int r = tc * 32 + n;
-        a[tc] = lc[buf][r * CPS + (c ^ swz(r))];
-      }
-#pragma unroll
-      for (int tp = 0; tp < 2; ++tp) {
-        const int r = wave * 64 + tp * 32 + n;
-        bx[tp] = lx[buf][r * CPS + (c ^ swz(r))];
-      }
-#pragma unroll
-      for (int tp = 0; tp < 2; ++tp)
-#pragma unroll
-        for (int tc = 0; tc < 4; ++tc) acc[tp][tc] = mfma32_chunk<DT>(a[tc], bx[tp], acc[tp][tc]);
-    }
-    if (do_norm && g == 0) {  // |x|^2 of point p0 + tid, in dimension order
-      const int r = tid;
-#pragma unroll
-      for (int c = 0; c < CPS; ++c) xs = chunk_sumsq<DT>(lx[buf][r * CPS + (c ^ swz(r))], xs);
-    }
-    if (ds == nds - 1) {  // this centroid block is complete: exact running arg-max
-      const int kb = (cb0 + g) * BC;
-#pragma unroll
-      for (int tp = 0; tp < 2; ++tp)
-#pragma unroll
-        for (int tc = 0; tc < 4; ++tc)
-#pragma unroll
-          for (int jj = 0; jj < 16; ++jj) {
-            const float v = acc[tp][tc][jj];
-            const bool gt = v > best[tp];
-            best[tp] = gt ? v : best[tp];
-            bidx[tp] = gt ? kb + tc * 32 + 8 * (jj >> 2) + (jj & 3) : bidx[tp];
-          }
-    }
-    if (s + 1 < S) tiled_store(pre, lx[buf ^ 1], lc[buf ^ 1], ln[buf ^ 1], tid);
-    __syncthreads();
+  for (int tp = 0; tp < 4; ++tp) {
+    best[tp] = -__builtin_inff();
+    code[tp] = 0;
+  }
+  TiledFrag f0, f1;
+  tiled_read(f0, buf0, c.loff0, wp, wc);
+  const int nq = nds / 4;  // nds % 4 == 0: every block starts in buffer 0
+  for (int g = 0; g < ncbw; ++g) {
+    tiled_init(acc, buf0, wc, h, Q);
+    const int s0 = g * nds;
+    const int full = g == ncbw - 1 ? nq - 1 : nq;  // quads with no stage past the end
+    for (int q = 0; q < full; ++q)
+      tiled_quad<DT, false>(c, s0 + 4 * q, buf0, buf1, buf2, buf3, acc, f0, f1);
+    if (full < nq) tiled_quad<DT, true>(c, s0 + 4 * full, buf0, buf1, buf2, buf3, acc, f0, f1);
+    tiled_epilogue(acc, best, code, (uint32_t)((cb0 + g) * (BC / 32) + wc * 4));
   }
 
-  // merge the two row halves of each point, then one atomic per point
+  // merge the two row halves of each point, then the two centroid halves of
+  // the workgroup (waves wc = 1 hand theirs over through LDS)
+  float* mv = reinterpret_cast<float*>(buf0);
+  int* mi = reinterpret_cast<int*>(buf0 + BP * 4);
+  float v[4];
+  int ix[4];
 #pragma unroll
-  for (int tp = 0; tp < 2; ++tp) {
-    float v = best[tp];
-    int i = bidx[tp] + 4 * h;
-    const float vo = __shfl_xor(v, 32);
+  for (int tp = 0; tp < 4; ++tp) {
+    const uint32_t jj = code[tp] & 15u;
+    const int i = (int)((code[tp] >> 4) * 32 + 8 * (jj >> 2) + 4 * h + (jj & 3));
+    const float vo = __shfl_xor(best[tp], 32);
     const int io = __shfl_xor(i, 32);
-    const bool take = (vo > v) || (vo == v && io < i);
-    v = take ? vo : v;
-    i = take ? io : i;
-    const int pt = p0 + wave * 64 + tp * 32 + n;
-    if (h == 0 && pt < N) {
-      const uint64_t key = ((uint64_t)ordered(v) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-      atomicMax((unsigned long long*)&keys[(size_t)b * N + pt], (unsigned long long)key);
+    const bool take = (vo > best[tp]) || (vo == best[tp] && io < i);
+    v[tp] = take ? vo : best[tp];
+    ix[tp] = take ? io : i;
+  }
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int tp = 0; tp < 4; ++tp) {
+      mv[wp * 128 + tp * 32 + n] = v[tp];
+      mi[wp * 128 + tp * 32 + n] = ix[tp];
     }
   }
-  if (do_norm && p0 + tid < N) xnorm[(size_t)b * N + p0 + tid] = xs;
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int tp = 0; tp < 4; ++tp) {
+      const int r = wp * 128 + tp * 32 + n;
+      const float vo = mv[r];
+      const int io = mi[r];
+      const bool take = (vo > v[tp]) || (vo == v[tp] && io < ix[tp]);
+      const float vv = take ? vo : v[tp];
+      const int ii = take ? io : ix[tp];
+      if (r <= c.last) {
+        const uint64_t key = ((uint64_t)ordered(vv) << 32) | (uint64_t)(0xffffffffu - (uint32_t)ii);
+        atomicMax((unsigned long long*)&keys[(size_t)b * N + p0 + r], (unsigned long long)key);
+      }
+    }
+  }
+}
+
+// Squared norms of the points, one wave per row: lane-strided, then a fixed
+// xor butterfly (the same bits on every call).
+template <int DT>
+__global__ __launch_bounds__(256) void row_norm_kernel(const uint4* __restrict__ X, int64_t rows,
+                                                       int RC, float* __restrict__ xnorm) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const uint4* row = X + r * RC;
+  float ss = 0.f;
+  for (int cc = lane; cc < RC; cc += 64) ss = chunk_sumsq<DT>(row[cc], ss);
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
+  if (lane == 0) xnorm[r] = ss;
 }
 
 __global__ __launch_bounds__(256) void fill_keys_kernel(uint64_t* __restrict__ keys, int64_t n) {
@@ -209,52 +372,73 @@ __global__ __launch_bounds__(256) void fill_keys_kernel(uint64_t* __restrict__ k
   if (i < n) keys[i] = 0;
 }
 
-// idx, min_dist and per-block objective partials from the keys.
+// idx, min_dist and per-block objective partials from the keys; a decode
+// block is a point block of the tiled kernel, so Q is recomputed from the
+// same norms.
 __global__ __launch_bounds__(256) void decode_keys_kernel(const uint64_t* __restrict__ keys,
                                                           const float* __restrict__ xnorm, int N,
                                                           int32_t* __restrict__ idx,
                                                           float* __restrict__ min_dist,
                                                           double* __restrict__ objpart) {
   __shared__ double s[256];
+  __shared__ float lds_q[4];
   const int b = blockIdx.y;
-  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
+  const int i = blockIdx.x * 256 + t;
+  const float xn = i < N ? xnorm[(size_t)b * N + i] : 0.f;
+  float xm = xn;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) xm = __builtin_fmaxf(xm, __shfl_xor(xm, m));
+  if (lane == 0) lds_q[t >> 6] = xm;
+  __syncthreads();
+  const float Q =
+      block_q(__builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])));
   double md = 0.0;
   if (i < N) {
     const uint64_t key = keys[(size_t)b * N + i];
     const float v = unordered((uint32_t)(key >> 32));
-    const float d = __builtin_fmaxf(__builtin_fmaf(-2.f, v, xnorm[(size_t)b * N + i]), 0.f);
+    const float d = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Q, xn), 0.f);
     idx[(size_t)b * N + i] = (int32_t)(0xffffffffu - (uint32_t)key);
     min_dist[(size_t)b * N + i] = d;
     md = d;
   }
-  s[threadIdx.x] = md;
+  s[t] = md;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
+    if (t < w) s[t] += s[t + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) objpart[(size_t)b * gridDim.x + blockIdx.x] = s[0];
+  if (t == 0) objpart[(size_t)b * gridDim.x + blockIdx.x] = s[0];
 }
 
 hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s) {
+  if (D % (4 * DC) != 0 || w.Kp % BC != 0) return hipErrorInvalidValue;
   const int64_t nk = B * N;
   fill_keys_kernel<<<dim3((unsigned)((nk + 255) / 256)), 256, 0, s>>>(w.keys, nk);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int RC = (int)(D / 8);
+  if (dt == DT_BF16)
+    row_norm_kernel<DT_BF16><<<dim3((unsigned)((nk + 3) / 4)), 256, 0, s>>>((const uint4*)X, nk, RC,
+                                                                          w.xnorm);
+  else
+    row_norm_kernel<DT_F16><<<dim3((unsigned)((nk + 3) / 4)), 256, 0, s>>>((const uint4*)X, nk, RC,
+                                                                         w.xnorm);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   const int npb = (int)((N + BP - 1) / BP);
   const int ncb = (int)(w.Kp / BC);
   const int ncbg = (ncb + TILED_CBG - 1) / TILED_CBG;
-  const int npb8 = (npb + 7) / 8 * 8;
-  const dim3 grid((unsigned)(npb8 * ncbg), (unsigned)B);
+  const int npb64 = (npb + 63) / 64 * 64;  // whole super-tiles on every XCD
+  const dim3 grid((unsigned)(npb64 * ncbg), (unsigned)B);
   if (dt == DT_BF16)
     assign_tiled_kernel<DT_BF16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
-                                                      w.cinit, (int)N, (int)D, (int)w.Kp, npb,
-                                                      ncbg, w.keys, w.xnorm);
+                                                      w.cinit, w.xnorm, (int)N, (int)D, (int)w.Kp,
+                                                      npb, ncbg, w.keys);
   else
     assign_tiled_kernel<DT_F16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
-                                                     w.cinit, (int)N, (int)D, (int)w.Kp, npb,
-                                                     ncbg, w.keys, w.xnorm);
+                                                     w.cinit, w.xnorm, (int)N, (int)D, (int)w.Kp,
+                                                     npb, ncbg, w.keys);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   decode_keys_kernel<<<dim3((unsigned)w.n_assign_blocks, (unsigned)B), 256, 0, s>>>(
       w.keys, w.xnorm, (int)N, idx, min_dist, w.objpart);

@@ -79,12 +79,16 @@ inline bool assign_resident_ok(int dt, int64_t D) {
 }
 inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D >= 512; }
 inline bool assign_ok(int dt, int64_t D) { return assign_resident_ok(dt, D) || assign_tiled(dt, D); }
-// Tiled kernel: 128-point x 128-centroid tiles, TILED_CBG centroid blocks per workgroup.
-constexpr int TILED_BP = 128, TILED_BC = 128, TILED_CBG = 8;
+// Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
+// workgroup; its centroids are padded to whole blocks.
+constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 4;
+inline int64_t kpad_for(int dt, int64_t D, int64_t K) {
+  return assign_tiled(dt, D) ? (K + TILED_BC - 1) / TILED_BC * TILED_BC : kpad(K);
+}
 
 // ---- workspace layout -------------------------------------------------------
 struct Workspace {
-  void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad(K))
+  void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad_for(dt, D, K))
   float* cinit;    // [B,Kp]   -1/2 * squared norm of each rounded centroid
   double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
   int32_t* rhist;  // [B,R,n_sort_chunks] radix histograms, then run starts (R <= 256)
