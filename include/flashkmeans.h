@@ -58,7 +58,9 @@ typedef enum {
 /*
  * Bytes of device workspace that kmeans_assign, kmeans_update and
  * kmeans_lloyd need for these sizes (one size serves all three).  Returns 0
- * for arguments that those calls would reject.  Pure host arithmetic.
+ * for arguments that those calls would reject.  Pure host arithmetic.  For
+ * fixed B, D, K and dtype it never decreases as N grows, so a workspace sized
+ * for N serves every smaller N.
  */
 size_t kmeans_workspace_bytes(int64_t B, int64_t N, int64_t D, int64_t K, int xdtype);
 

@@ -44,6 +44,10 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   w.perm = (int32_t*)take((size_t)(B * N) * 4);
   w.carry = (float*)take((size_t)(red_slices_bound(B, N) * 2 * D) * 4);
   w.sums = (float*)take((size_t)(B * K * D) * 4);
+  const bool sk = smallk_ok(dt, D, K);
+  w.n_sk_chunks = (N + SMALLK_CH - 1) / SMALLK_CH;
+  w.partial = (float*)take(sk ? (size_t)(B * w.n_sk_chunks * K * D) * 4 : 0);
+  w.pcount = (int32_t*)take(sk ? (size_t)(B * w.n_sk_chunks * K) * 4 : 0);
   const bool tiled = assign_tiled(dt, D);
   w.keys = (uint64_t*)take(tiled ? (size_t)(B * N) * 8 : 0);
   w.xnorm = (float*)take(tiled ? (size_t)(B * N) * 4 : 0);

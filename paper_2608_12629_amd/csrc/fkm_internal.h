@@ -50,6 +50,14 @@ inline int64_t red_slices_bound(int64_t B, int64_t N) {
   const int64_t cap = coarse > RED_WAVES ? coarse : RED_WAVES;
   return fine < cap ? fine : cap;
 }
+// Small-K update: chunks of SMALLK_CH points sorted in LDS, per-chunk
+// partial sums; used when K <= 512 (fp32) or 256 (16-bit), so the partials
+// stay within a quarter of the rows they sum, and K * D <= SMALLK_MAX_KD.
+constexpr int SMALLK_CH = 2048, SMALLK_MAX_K = 512;
+constexpr int64_t SMALLK_MAX_KD = 16384;
+inline bool smallk_ok(int dt, int64_t D, int64_t K) {
+  return K <= (dt == DT_F32 ? 512 : 256) && K * D <= SMALLK_MAX_KD;
+}
 // Limits of this build.
 constexpr int64_t MAX_K = 65536;   // two radix passes of at most 8 bits
 constexpr int64_t MAX_D = 2048;
@@ -101,9 +109,11 @@ struct Workspace {
   int32_t* perm;   // [B,N] point ids sorted by cluster
   float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by slice ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
+  float* partial;  // [B,n_sk_chunks,K,D] per-chunk cluster sums (small-K update only)
+  int32_t* pcount; // [B,n_sk_chunks,K] per-chunk cluster counts (small-K update only)
   uint64_t* keys;  // [B,N] best (score, index) of each point (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
-  int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr;
+  int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr, n_sk_chunks;
   size_t total;
 };
 

@@ -31,10 +31,11 @@ __device__ __forceinline__ int digit_of(int key, int shift, int R) { return (key
 
 static_assert(RADIX_MAX_R == 256, "the scans give each bin one thread of a 256-thread workgroup");
 
-// Exclusive scan of one value per thread over a 256-thread workgroup: a
-// shuffle scan inside each wave, then the four wave totals through `wsum`
-// (one barrier).  Returns the exclusive prefix; `total` gets the sum.
-__device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
+// Exclusive scan of one value per thread over a workgroup of W waves: a
+// shuffle scan inside each wave, then the wave totals through `wsum` (one
+// barrier).  Returns the exclusive prefix; `total` gets the sum.
+template <int W>
+__device__ __forceinline__ int block_scan(int v, int* wsum, int& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int x = v;
 #pragma unroll
@@ -47,12 +48,15 @@ __device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
   int pre = 0;
   total = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < W; ++i) {
     const int s = wsum[i];
     pre += i < w ? s : 0;
     total += s;
   }
   return pre + x - v;
+}
+__device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
+  return block_scan<4>(v, wsum, total);
 }
 
 }  // namespace
@@ -421,6 +425,207 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Small-K update (smallk_ok: few clusters, K * D small): no global sort.  A
+// workgroup of 16 waves takes SMALLK_CH consecutive points of one instance,
+// sorts them by cluster id in LDS (stable: per-wave counts, a scan over
+// clusters, then a ballot multi-split ranking in point order) and sums each
+// cluster's rows in that order (rows strided over lane groups, then a xor
+// butterfly) into the chunk's partial [K, D] and count.  smallk_combine adds
+// a cluster's partials in chunk order and divides.  X is read once; no
+// floating-point atomics; every sum has a fixed order.
+template <int DT, int LPR, int CPLR>
+__global__ __launch_bounds__(1024) void smallk_partials_kernel(
+    const uint4* __restrict__ X, const int32_t* __restrict__ idx, int N, int K, int dbits, int nch,
+    float* __restrict__ partial, int32_t* __restrict__ pcount) {
+  constexpr int E = Row<DT>::per16;
+  constexpr int RC = LPR * CPLR;
+  constexpr int D = RC * E;
+  constexpr int RPW = 64 / LPR;
+  constexpr int NA = CPLR * E;
+  constexpr int U = CPLR >= 8 ? 1 : 8 / CPLR;  // rows in flight per lane (4 waves per SIMD)
+  constexpr int W = 16, CH = SMALLK_CH, PER = CH / W / 64;
+  static_assert(PER * 64 * W == CH, "whole 64-entry steps per wave");
+  __shared__ int cnt[W][SMALLK_MAX_K];  // per-wave counts, then per-wave run starts
+  __shared__ int kst[SMALLK_MAX_K + 1];  // cluster run starts within the chunk
+  __shared__ int plist[CH];              // chunk offsets of the points, sorted by cluster
+  __shared__ int wsum[W];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int ch = blockIdx.x, b = blockIdx.y;
+  const int i0 = ch * CH;
+  const int nin = min(CH, N - i0);
+  const int32_t* ib = idx + (size_t)b * N + i0;
+
+  int k[PER];
+#pragma unroll
+  for (int s = 0; s < PER; ++s) {
+    const int e = (w * PER + s) * 64 + lane;
+    k[s] = e < nin ? ib[e] : -1;
+  }
+  for (int r = t; r < W * SMALLK_MAX_K; r += 1024) (&cnt[0][0])[r] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < PER; ++s)
+    if ((unsigned)k[s] < (unsigned)K) atomicAdd(&cnt[w][k[s]], 1);  // integer: exact
+  __syncthreads();
+  int c16[W], tot = 0;
+#pragma unroll
+  for (int ww = 0; ww < W; ++ww) {
+    c16[ww] = t < K ? cnt[ww][t] : 0;
+    tot += c16[ww];
+  }
+  int total;
+  const int ex = block_scan<W>(tot, wsum, total);
+  if (t < K) {
+    kst[t] = ex;
+    int run = ex;
+#pragma unroll
+    for (int ww = 0; ww < W; ++ww) {
+      cnt[ww][t] = run;
+      run += c16[ww];
+    }
+  }
+  if (t == 0) kst[K] = total;
+  __syncthreads();
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int s = 0; s < PER; ++s) {
+    const bool valid = (unsigned)k[s] < (unsigned)K;
+    const int dg = valid ? k[s] : 0;
+    uint64_t match = __ballot(valid);
+    for (int bit = 0; bit < dbits; ++bit) {
+      const int on = (dg >> bit) & 1;
+      const uint64_t bb = __ballot(on);
+      match &= bb ^ (uint64_t)(int64_t)(on - 1);
+    }
+    if (valid) {
+      const int rank = __popcll(match & below);
+      const int start = cnt[w][dg];
+      if (rank == 0) cnt[w][dg] = start + __popcll(match);
+      plist[start + rank] = (w * PER + s) * 64 + lane;
+    }
+  }
+  __syncthreads();
+
+  const uint4* xb = X + ((size_t)b * N + i0) * RC;
+  const int r = lane / LPR, q = lane % LPR;
+  float* pb = partial + ((size_t)b * nch + ch) * K * D;
+  for (int kk = w; kk < K; kk += W) {
+    const int s0 = kst[kk], s1 = kst[kk + 1];
+    float acc[NA];
+#pragma unroll
+    for (int a = 0; a < NA; ++a) acc[a] = 0.f;
+    for (int j = s0 + r; j < s1; j += U * RPW) {
+      uint4 v[U][CPLR];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jj = j + u * RPW;
+        if (jj < s1) {
+          const uint4* row = xb + (size_t)plist[jj] * RC + q * CPLR;
+#pragma unroll
+          for (int c = 0; c < CPLR; ++c) v[u][c] = row[c];
+        } else {
+#pragma unroll
+          for (int c = 0; c < CPLR; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int c = 0; c < CPLR; ++c) Row<DT>::add(v[u][c], acc + c * E);
+    }
+#pragma unroll
+    for (int msk = LPR; msk < 64; msk <<= 1)
+#pragma unroll
+      for (int a = 0; a < NA; ++a) acc[a] += __shfl_xor(acc[a], msk);
+    if (r == 0) {
+#pragma unroll
+      for (int c = 0; c < CPLR; ++c) {
+        float4* d4 = reinterpret_cast<float4*>(pb + (size_t)kk * D + (q * CPLR + c) * E);
+#pragma unroll
+        for (int e = 0; e < E; e += 4)
+          d4[e / 4] = make_float4(acc[c * E + e], acc[c * E + e + 1], acc[c * E + e + 2],
+                                  acc[c * E + e + 3]);
+      }
+    }
+    if (lane == 0) pcount[((size_t)b * nch + ch) * K + kk] = s1 - s0;
+  }
+}
+
+// One workgroup per cluster: the count (integer sum over chunks), then per
+// 4 dimensions the partials added in chunk order and divided by the count; an
+// empty cluster keeps its previous centroid.
+__global__ __launch_bounds__(256) void smallk_combine_kernel(
+    const float* __restrict__ partial, const int32_t* __restrict__ pcount, const float* C_prev,
+    int K, int D, int nch, float* C_out, int32_t* __restrict__ counts) {
+  __shared__ int wsum[4];
+  const int k = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  int n = 0;
+  for (int c = t; c < nch; c += 256) n += pcount[((size_t)b * nch + c) * K + k];
+  int total;
+  block_scan256(n, wsum, total);
+  if (t == 0) counts[(size_t)b * K + k] = total;
+  const int D4 = D / 4;
+  const size_t rowoff = ((size_t)b * K + k) * D;
+  const float fn = (float)total;
+  for (int d = t; d < D4; d += 256) {
+    float4 o;
+    if (total == 0) {
+      o = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+    } else {
+      float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int c = 0; c < nch; ++c) {
+        const float4 v = reinterpret_cast<const float4*>(
+            partial + (((size_t)b * nch + c) * K + k) * D)[d];
+        sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
+      }
+      o = make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
+    }
+    reinterpret_cast<float4*>(C_out + rowoff)[d] = o;
+  }
+}
+
+template <int DT, int LPR, int CPLR>
+static void launch_smallk(const void* X, const int32_t* idx, const Workspace& w, int64_t B,
+                          int64_t N, int64_t K, int dbits, hipStream_t s) {
+  smallk_partials_kernel<DT, LPR, CPLR><<<dim3((unsigned)w.n_sk_chunks, (unsigned)B), 1024, 0, s>>>(
+      (const uint4*)X, idx, (int)N, (int)K, dbits, (int)w.n_sk_chunks, w.partial, w.pcount);
+}
+
+template <int DT>
+static hipError_t launch_smallk_dt(const void* X, const int32_t* idx, const Workspace& w, int64_t B,
+                                   int64_t N, int64_t D, int64_t K, int dbits, hipStream_t s) {
+  const int64_t rc = D * dt_bytes(DT) / 16;  // 16-byte chunks per row
+  switch (rc) {
+    case 4: launch_smallk<DT, 4, 1>(X, idx, w, B, N, K, dbits, s); break;
+    case 8: launch_smallk<DT, 8, 1>(X, idx, w, B, N, K, dbits, s); break;
+    case 16: launch_smallk<DT, 16, 1>(X, idx, w, B, N, K, dbits, s); break;
+    case 32: launch_smallk<DT, 32, 1>(X, idx, w, B, N, K, dbits, s); break;
+    case 64: launch_smallk<DT, 64, 1>(X, idx, w, B, N, K, dbits, s); break;
+    case 128: launch_smallk<DT, 64, 2>(X, idx, w, B, N, K, dbits, s); break;
+    case 256: launch_smallk<DT, 64, 4>(X, idx, w, B, N, K, dbits, s); break;
+    case 512: launch_smallk<DT, 64, 8>(X, idx, w, B, N, K, dbits, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+static hipError_t launch_update_smallk(const void* X, int dt, const int32_t* idx,
+                                       const float* C_prev, const Workspace& w, int64_t B,
+                                       int64_t N, int64_t D, int64_t K, float* C_out,
+                                       int32_t* counts, hipStream_t s) {
+  int dbits = 0;
+  while ((1ll << dbits) < K) ++dbits;
+  hipError_t e;
+  if (dt == DT_BF16) e = launch_smallk_dt<DT_BF16>(X, idx, w, B, N, D, K, dbits, s);
+  else if (dt == DT_F16) e = launch_smallk_dt<DT_F16>(X, idx, w, B, N, D, K, dbits, s);
+  else e = launch_smallk_dt<DT_F32>(X, idx, w, B, N, D, K, dbits, s);
+  if (e != hipSuccess) return e;
+  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
+      w.partial, w.pcount, C_prev, (int)K, (int)D, (int)w.n_sk_chunks, C_out, counts);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 template <int DT, int LPR, int CPLR>
 static void launch_segreduce(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t K,
                              hipStream_t s) {
@@ -485,6 +690,8 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
                          float* C_out, int32_t* counts, hipStream_t s) {
+  if (smallk_ok(dt, D, K))
+    return launch_update_smallk(X, dt, idx, C_prev, w, B, N, D, K, C_out, counts, s);
   hipError_t e;
   const int nch = (int)w.n_sort_chunks;
   int passes, d1, d2;

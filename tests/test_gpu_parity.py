@@ -125,6 +125,8 @@ SHAPES = [
     (1, 3000, 32, 65, "bf16"),        # D = 32
     (3, 2500, 64, 40, "f16"),         # batched, ragged
     (1, 300, 64, 300, "bf16"),        # K = N
+    (2, 6000, 128, 128, "bf16"),      # per-chunk update at K * D = 16384, ragged chunk
+    (1, 10000, 32, 512, "f32"),       # per-chunk update, fp32, 9-bit cluster ids
     (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
     (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
