@@ -1,22 +1,24 @@
 // assign.hip -- the assignment step of the Lloyd iteration (paper Section 5:
 // squared Euclidean distance of each point to all K centroids, then the
-// arg-min), fused so that the N x K distance matrix is never stored.
+// arg-min), fused so that the N x K distance matrix is never stored.  This
+// file holds the centroid preparation, the fp32 kernel, the objective pass
+// and the dispatch; the bf16/fp16 kernels are in assign_pipe.h (D <= 256) and
+// assign_tiled.hip (wider rows).
 //
-// For point x and centroid c the kernel maximises
+// For point x and centroid c the kernels maximise
 //     s(x, c) = <x, c^> - |c^|^2 / 2
 // which orders the centroids exactly as |x - c^|^2 = |x|^2 - 2 s(x, c) does
 // (|x|^2 is common to all of them).  c^ is the centroid rounded once to the
-// storage type of x; <x, c^> runs on the matrix cores (bf16/fp16 16x16x32 or
-// fp32 16x16x4 MFMA) with fp32 accumulation, and -|c^|^2 / 2 enters as the
-// accumulator's initial value, so the epilogue is a bare compare-and-select.
+// storage type of x; <x, c^> runs on the matrix cores with fp32 accumulation,
+// and -|c^|^2 / 2 enters as the accumulator's initial value.
 //
-// Layout of one MFMA tile: 16 centroids (A rows) x 16 points (B columns).
-// Lane l = 16 g + m supplies centroid row m and point column m for the
-// k-slice g (the k-to-lane map is the same for A and B, so any fixed split of
-// the D dimensions over the four lane groups gives the same contraction);
-// it receives accumulator rows 4 g .. 4 g + 3 of column m.  A lane therefore
-// keeps a running best over its own quarter of the centroids of one point,
-// and the four quarters are merged once at the end.
+// fp32 kernel layout, one 16x16x4 MFMA tile: 16 centroids (A rows) x 16
+// points (B columns).  Lane l = 16 g + m supplies centroid row m and point
+// column m for the k-slice g (the k-to-lane map is the same for A and B, so
+// any fixed split of the D dimensions over the four lane groups gives the same
+// contraction); it receives accumulator rows 4 g .. 4 g + 3 of column m.  A
+// lane therefore keeps a running best over its own quarter of the centroids
+// of one point, and the four quarters are merged once at the end.
 #include "fkm_device.h"
 
 namespace fkm {
@@ -62,21 +64,23 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, 
 // ---------------------------------------------------------------------------
 // Resident-X assignment.  CPL = 16-byte chunks of one point held by one lane
 // (the point's row is split over the four lane groups), NSUB = 16-point MFMA
-// column tiles per wave.
+// column tiles per wave.  A centroid row of RC chunks sits in LDS at a
+// power-of-two stride RCP >= RC, XOR-swizzled within it.
 template <int DT, int CPL, int NSUB>
 __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
     int N, int K, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
     double* __restrict__ objpart) {
   constexpr int RC = 4 * CPL;              // 16-byte chunks per row
-  constexpr int SWZ = RC < 16 ? RC - 1 : 15;
+  constexpr int RCP = pow2_at_least(RC);   // chunk slots per LDS row
+  constexpr int SWZ = RCP < 16 ? RCP - 1 : 15;
   constexpr int TCS = ASSIGN_TCS;
   constexpr int PPW = 16 * NSUB;           // points per wave
   constexpr int PPB = 4 * PPW;             // points per workgroup
   constexpr int LOADS = TCS * RC / ASSIGN_THREADS;  // chunks per thread per stage
   static_assert(LOADS * ASSIGN_THREADS == TCS * RC, "stage must split evenly");
 
-  __shared__ uint4 lds_c[2][TCS * RC];
+  __shared__ uint4 lds_c[2][TCS * RCP];
   __shared__ __attribute__((aligned(16))) float lds_n[2][TCS];
   __shared__ double lds_obj[4];
 
@@ -128,7 +132,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     for (int u = 0; u < LOADS; ++u) {
       const int q = tid + u * ASSIGN_THREADS;
       const int r = q / RC, c = q % RC;
-      lds_c[buf][r * RC + (c ^ (r & SWZ))] = pre[u];
+      lds_c[buf][r * RCP + (c ^ (r & SWZ))] = pre[u];
     }
     if (tid < TCS) lds_n[buf][tid] = pren;
   };
@@ -153,7 +157,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
       const f32x4 cin = *reinterpret_cast<const f32x4*>(&lds_n[buf][tile * 16 + 4 * g]);
       uint4 a[CPL];
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) a[c] = lds_c[buf][row * RC + ((g * CPL + c) ^ (row & SWZ))];
+      for (int c = 0; c < CPL; ++c) a[c] = lds_c[buf][row * RCP + ((g * CPL + c) ^ (row & SWZ))];
       const int kcode = st * TCS + tile * 16;  // + 4 g + j is the centroid index
 #pragma unroll
       for (int p = 0; p < NSUB; ++p) {
@@ -202,309 +206,6 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
 }
 
-// ---------------------------------------------------------------------------
-// Resident-X assignment on 32x32x16 bf16/fp16 MFMA tiles, software-pipelined.
-//
-// Tile layout: 32 centroids (A rows) x 32 points (B columns) per instruction.
-// Lane l = 32 h + n supplies point column n and centroid row n for the
-// k-slice h (each lane group holds one contiguous half of the D dimensions)
-// and receives accumulator rows 8 q + 4 h + r (q, r = 0..3) of column n.
-// Each wave keeps NSUB 32-point column tiles in registers for the whole
-// kernel; centroids stream through LDS in stages of TCS rows (four tiles, or
-// two for 512-byte rows, so that two stage buffers of two workgroups fit).
-//
-// Staging.  Each stage goes from L2 straight into LDS (global_load_lds, 16
-// bytes per lane, no registers, no LDS store instructions): lane l of a wave
-// fills LDS slot base + 16 l, so each lane fetches the centroid chunk that the
-// swizzled layout puts in its slot.  The two stage buffers are separate LDS
-// arrays: the compiler then sees that a load in flight into one buffer cannot
-// alias the reads of the other and does not wait for it before reading.
-//
-// Pipelining.  On this GPU the matrix pipe and the vector ALU overlap only
-// within one wave's instruction stream (a wave that only issues vector
-// instructions does not run beside another wave's MFMAs).  So the MFMAs of
-// tile t and the epilogue of tile t-1 are written into the same basic block,
-// on two accumulator sets, for the scheduler to interleave; NSUB independent
-// accumulation chains keep the matrix pipe fed, and each MFMA is followed by
-// a few vector instructions and one LDS read of a later A operand.
-//
-// Epilogue.  The accumulator starts at -|c^|^2/2 - Q, with Q a bound on
-// |x|^2/2 over the workgroup's points plus a margin, so every score
-// s' = <x, c^> - |c^|^2/2 - Q is strictly negative and orders the centroids
-// like the distance does.  The lane's position j = 4 q + r is written into the
-// 4 low mantissa bits of each score (one and-or), a max3 tree picks the
-// tile's best (for negative floats larger low bits mean more negative, so on
-// equal upper bits the lowest position wins), and a strict compare on the
-// masked value keeps the earliest tile.  Scores within 16 ulp of each other
-// therefore count as ties and go to the lowest index; nothing else changes.
-// Padding rows score -FLT_MAX (an infinity with position bits would be a
-// signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
-typedef __attribute__((address_space(1))) void global_void;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Per-lane offsets, fixed for the whole kernel.
-template <int CPL, int LOADS>
-struct PipeOffsets {
-  int src[LOADS];    // chunk of a stage that lands in LDS slot tid + u * 256
-  int a[CPL];        // byte offset of chunk h * CPL + c of centroid row n of tile 0
-  int n_store;       // byte offset of the score slot written by this thread
-  int n_read;        // byte offset of the first score read by this lane (rows 4 h .. 4 h + 3)
-};
-
-// Stage = TCS centroid rows of RC 16-byte chunks (XOR-swizzled), then TCS scores.
-template <int CPL>
-struct PipeLayout {
-  static constexpr int TCS = CPL <= 8 ? 128 : 64, RC = 2 * CPL, TILES = TCS / 32;
-  static constexpr int SWZ = RC < 16 ? RC - 1 : 15;
-  static constexpr int CHUNKS = TCS * RC * 16;          // bytes of centroid chunks
-  static constexpr int STAGE = CHUNKS + TCS * 4;         // bytes per stage buffer
-  static constexpr int TILE = 32 * RC * 16;              // bytes per tile of chunks
-};
-
-template <int CPL, int LOADS>
-__device__ __forceinline__ void pipe_offsets(PipeOffsets<CPL, LOADS>& o, int tid, int n, int h) {
-  using L = PipeLayout<CPL>;
-#pragma unroll
-  for (int u = 0; u < LOADS; ++u) {  // slot s holds row s / RC, chunk (s % RC) ^ (row & SWZ)
-    const int sl = tid + u * ASSIGN_THREADS;
-    const int r = sl / L::RC;
-    o.src[u] = r * L::RC + ((sl % L::RC) ^ (r & L::SWZ));
-  }
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) o.a[c] = (n * L::RC + ((h * CPL + c) ^ (n & L::SWZ))) * 16;
-  o.n_store = L::CHUNKS + (tid & (L::TCS - 1)) * 4;
-  o.n_read = L::CHUNKS + 16 * h;
-}
-
-// LDS accesses at a per-lane offset plus a compile-time byte offset.
-template <typename T>
-__device__ __forceinline__ T& lds_at(char* base, int lane_off, int imm) {
-  return *reinterpret_cast<T*>(base + lane_off + imm);
-}
-
-// Start stage `st` on its way into `buf` (complete after the wave's next
-// vmcnt(0) wait and a barrier) and fetch this thread's score for it.
-template <int CPL, int LOADS>
-__device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat,
-                                                  const float* __restrict__ cinit, int st, int tid,
-                                                  const PipeOffsets<CPL, LOADS>& o, char* buf) {
-  using L = PipeLayout<CPL>;
-  const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-#pragma unroll
-  for (int u = 0; u < LOADS; ++u)
-    __builtin_amdgcn_global_load_lds((global_void*)(src + o.src[u]),
-                                     (lds_void*)(buf + (u * ASSIGN_THREADS + wave * 64) * 16), 16, 0,
-                                     0);
-  return cinit[st * L::TCS + (tid & (L::TCS - 1))];
-}
-
-// The MFMAs of one 32-centroid tile into acc; each chain starts from the scores' init.
-template <int DT, int TILE, int CPL, int NSUB, int LOADS>
-__device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 (&xr)[NSUB][CPL],
-                                               char* buf, const PipeOffsets<CPL, LOADS>& o) {
-  using L = PipeLayout<CPL>;
-  f32x16 cin;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 v = lds_at<f32x4>(buf, o.n_read, (TILE * 32 + 8 * q) * 4);
-    cin[4 * q + 0] = v[0];
-    cin[4 * q + 1] = v[1];
-    cin[4 * q + 2] = v[2];
-    cin[4 * q + 3] = v[3];
-  }
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const uint4 a = lds_at<uint4>(buf, o.a[c], TILE * L::TILE);
-#pragma unroll
-    for (int p = 0; p < NSUB; ++p) acc[p] = mfma32_chunk<DT>(a, xr[p][c], c == 0 ? cin : acc[p]);
-  }
-}
-
-// Packed-key arg-max of one tile into the running (best, code) of each column tile.
-template <int NSUB>
-__device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_t tcode,
-                                              float (&best)[NSUB], uint32_t (&code)[NSUB]) {
-#pragma unroll
-  for (int p = 0; p < NSUB; ++p) {
-    float k[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-      k[j] = __uint_as_float((__float_as_uint(acc[p][j]) & ~15u) | (uint32_t)j);
-    const float t0 = __builtin_fmaxf(__builtin_fmaxf(k[0], k[1]), k[2]);
-    const float t1 = __builtin_fmaxf(__builtin_fmaxf(k[3], k[4]), k[5]);
-    const float t2 = __builtin_fmaxf(__builtin_fmaxf(k[6], k[7]), k[8]);
-    const float t3 = __builtin_fmaxf(__builtin_fmaxf(k[9], k[10]), k[11]);
-    const float t4 = __builtin_fmaxf(__builtin_fmaxf(k[12], k[13]), k[14]);
-    const float u0 = __builtin_fmaxf(__builtin_fmaxf(t0, t1), t2);
-    const float u1 = __builtin_fmaxf(__builtin_fmaxf(t3, t4), k[15]);
-    const uint32_t mb = __float_as_uint(__builtin_fmaxf(u0, u1));
-    const float mm = __uint_as_float(mb & ~15u);
-    const bool gt = mm > best[p];
-    best[p] = gt ? mm : best[p];
-    code[p] = gt ? ((mb & 15u) | tcode) : code[p];
-  }
-}
-
-// One stage in `cur`: start the next stage into `nxt`, run the stage's tiles
-// (tile i on one accumulator set beside the epilogue of tile i-1 on the
-// other), store the next stage's scores, then wait for the loads and sync.
-template <int DT, int CPL, int NSUB, int LOADS>
-__device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
-                                           const uint4 (&xr)[NSUB][CPL], char* cur, char* nxt,
-                                           const PipeOffsets<CPL, LOADS>& o, const u32x4* chat,
-                                           const float* cinit, float Q, int tid,
-                                           uint32_t& prev_code, float (&best)[NSUB],
-                                           uint32_t (&code)[NSUB]) {
-  using L = PipeLayout<CPL>;
-  const float nn = pipe_issue_stage<CPL, LOADS>(chat, cinit, next, tid, o, nxt);
-  // issue the prefetch first: left to the scheduler it drifts into the middle
-  // of the stage and the wait at the end stalls on it
-  __builtin_amdgcn_sched_barrier(0);
-  const uint32_t tb = (uint32_t)(L::TILES * st);
-  pipe_mfma_tile<DT, 0, CPL, NSUB, LOADS>(accB, xr, cur, o);
-  pipe_epilogue<NSUB>(accA, prev_code, best, code);
-  pipe_mfma_tile<DT, 1, CPL, NSUB, LOADS>(accA, xr, cur, o);
-  pipe_epilogue<NSUB>(accB, tb << 4, best, code);
-  if constexpr (L::TILES == 4) {
-    pipe_mfma_tile<DT, 2, CPL, NSUB, LOADS>(accB, xr, cur, o);
-    pipe_epilogue<NSUB>(accA, (tb + 1) << 4, best, code);
-    pipe_mfma_tile<DT, 3, CPL, NSUB, LOADS>(accA, xr, cur, o);
-    pipe_epilogue<NSUB>(accB, (tb + 2) << 4, best, code);
-  }
-  prev_code = (tb + L::TILES - 1) << 4;
-  lds_at<float>(nxt, o.n_store, 0) = nn - Q;
-  // interleave: the first few LDS reads, then one MFMA, a few vector
-  // instructions and one LDS read, repeated
-  __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-#pragma unroll
-  for (int i = 0; i < L::TILES * NSUB * CPL; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-}
-
-template <int DT, int CPL, int NSUB>
-__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
-    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
-    int N, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
-    double* __restrict__ objpart) {
-  static_assert(DT != DT_F32, "16-bit storage types only");
-  using L = PipeLayout<CPL>;
-  static_assert(ASSIGN_KPAD % L::TCS == 0, "K is padded to whole stages");
-  constexpr int RC = L::RC;
-  constexpr int PPW = 32 * NSUB;           // points per wave
-  constexpr int PPB = 4 * PPW;             // points per workgroup
-  constexpr int LOADS = L::TCS * RC / ASSIGN_THREADS;
-  static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * RC, "stage must split evenly");
-
-  __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
-  __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
-  __shared__ float lds_q[4];
-  __shared__ double lds_obj[4];
-
-  const int b = blockIdx.y;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int n = lane & 31, h = lane >> 5;
-  X += (size_t)b * N * RC;
-  const u32x4* chat4 = reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * RC;
-  cinit += (size_t)b * Kp;
-  idx += (size_t)b * N;
-  min_dist += (size_t)b * N;
-  const int nst = Kp / L::TCS;
-
-  PipeOffsets<CPL, LOADS> o;
-  pipe_offsets<CPL, LOADS>(o, tid, n, h);
-  const float n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
-
-  const int pbase = blockIdx.x * PPB + wave * PPW;
-  uint4 xr[NSUB][CPL];
-  float xn[NSUB];
-  float xmax = 0.f;
-#pragma unroll
-  for (int p = 0; p < NSUB; ++p) {
-    const int pt = pbase + p * 32 + n;
-    const bool ok = pt < N;
-    float ss = 0.f;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      xr[p][c] = ok ? X[(size_t)pt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
-      ss = chunk_sumsq<DT>(xr[p][c], ss);
-    }
-    ss += __shfl_xor(ss, 32);
-    xn[p] = ss;
-    xmax = __builtin_fmaxf(xmax, ss);
-  }
-#pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) xmax = __builtin_fmaxf(xmax, __shfl_xor(xmax, msk));
-  if (lane == 0) lds_q[wave] = xmax;
-  __syncthreads();
-  // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding)
-  const float Q = __builtin_fmaf(
-      0.5f * __builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])),
-      1.0f + 0x1p-8f, 1e-30f);
-
-  float best[NSUB];
-  uint32_t code[NSUB];
-#pragma unroll
-  for (int p = 0; p < NSUB; ++p) {
-    best[p] = -__builtin_inff();
-    code[p] = 0;
-  }
-  // accA holds the previous tile; before the first tile it is a dummy at the
-  // most negative score, which every real score replaces
-  f32x16 accA[NSUB], accB[NSUB];
-#pragma unroll
-  for (int p = 0; p < NSUB; ++p)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) accA[p][j] = -0x1.fffffep127f;
-  uint32_t prev_code = 0;
-
-  lds_at<float>(buf0, o.n_store, 0) = n0 - Q;
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  int st = 0;
-  for (; st + 2 <= nst; st += 2) {   // two stages per trip: each buffer is a fixed array
-    pipe_stage<DT, CPL, NSUB, LOADS>(st, st + 1, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q,
-                                     tid, prev_code, best, code);
-    pipe_stage<DT, CPL, NSUB, LOADS>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr, buf1,
-                                     buf0, o, chat4, cinit, Q, tid, prev_code, best, code);
-  }
-  if (st < nst)
-    pipe_stage<DT, CPL, NSUB, LOADS>(st, st, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q, tid,
-                                     prev_code, best, code);
-  pipe_epilogue<NSUB>(accA, prev_code, best, code);
-
-  double obj = 0.0;
-#pragma unroll
-  for (int p = 0; p < NSUB; ++p) {
-    float v = best[p];
-    const uint32_t j = code[p] & 15u;
-    int i = (int)((code[p] >> 4) * 32 + 8 * (j >> 2) + 4 * h + (j & 3));
-    const float vo = __shfl_xor(v, 32);
-    const int io = __shfl_xor(i, 32);
-    const bool take = (vo > v) || (vo == v && io < i);
-    v = take ? vo : v;
-    i = take ? io : i;
-    const int pt = pbase + p * 32 + n;
-    if (h == 0 && pt < N) {
-      const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Q, xn[p]), 0.f);
-      idx[pt] = i;
-      min_dist[pt] = md;
-      obj += (double)md;
-    }
-  }
-#pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) obj += __shfl_xor(obj, msk);
-  if (lane == 0) lds_obj[wave] = obj;
-  __syncthreads();
-  if (tid == 0)
-    objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
-}
 
 // Sum of one instance's workgroup partials in a fixed order, in fp64: thread t
 // sums partials t, t + 1024, ... (eight loads in flight), then a tree in LDS.
@@ -561,33 +262,16 @@ template <int DT>
 static hipError_t launch_resident_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
                                      int64_t D, int64_t K, int32_t* idx, float* min_dist,
                                      hipStream_t s) {
-  switch (D * dt_bytes(DT) / 64) {
+  if (D % 16 != 0) return hipErrorInvalidValue;
+  switch (D / 16) {  // chunks per lane
     case 1: return launch_resident<DT, 1>(X, w, B, N, K, idx, min_dist, s);
     case 2: return launch_resident<DT, 2>(X, w, B, N, K, idx, min_dist, s);
+    case 3: return launch_resident<DT, 3>(X, w, B, N, K, idx, min_dist, s);
     case 4: return launch_resident<DT, 4>(X, w, B, N, K, idx, min_dist, s);
+    case 5: return launch_resident<DT, 5>(X, w, B, N, K, idx, min_dist, s);
+    case 6: return launch_resident<DT, 6>(X, w, B, N, K, idx, min_dist, s);
+    case 7: return launch_resident<DT, 7>(X, w, B, N, K, idx, min_dist, s);
     case 8: return launch_resident<DT, 8>(X, w, B, N, K, idx, min_dist, s);
-    default: return hipErrorInvalidValue;
-  }
-}
-
-template <int DT, int CPL, int NSUB>
-static hipError_t launch_pipe(const void* X, const Workspace& w, int64_t B, int64_t N,
-                              int32_t* idx, float* min_dist, hipStream_t s) {
-  const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
-  assign_pipe_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
-      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)w.Kp, idx, min_dist, w.objpart);
-  return hipGetLastError();
-}
-
-// NSUB must agree with assign_nsub16(D).
-template <int DT>
-static hipError_t launch_pipe_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
-                                 int64_t D, int32_t* idx, float* min_dist, hipStream_t s) {
-  switch (D) {
-    case 32: return launch_pipe<DT, 2, 4>(X, w, B, N, idx, min_dist, s);
-    case 64: return launch_pipe<DT, 4, 4>(X, w, B, N, idx, min_dist, s);
-    case 128: return launch_pipe<DT, 8, 2>(X, w, B, N, idx, min_dist, s);
-    case 256: return launch_pipe<DT, 16, 1>(X, w, B, N, idx, min_dist, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -596,8 +280,8 @@ hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, i
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
   if (assign_tiled(dt, D)) return launch_assign_tiled(X, dt, w, B, N, D, idx, min_dist, s);
   if (!assign_resident_ok(dt, D)) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return launch_pipe_dt<DT_BF16>(X, w, B, N, D, idx, min_dist, s);
-  if (dt == DT_F16) return launch_pipe_dt<DT_F16>(X, w, B, N, D, idx, min_dist, s);
+  if (dt == DT_BF16) return launch_pipe_bf16(X, w, B, N, D, idx, min_dist, s);
+  if (dt == DT_F16) return launch_pipe_f16(X, w, B, N, D, idx, min_dist, s);
   return launch_resident_dt<DT_F32>(X, w, B, N, D, K, idx, min_dist, s);
 }
 

@@ -11,6 +11,7 @@ namespace fkm {
 enum Dt { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
 
 inline int dt_bytes(int dt) { return dt == DT_F32 ? 4 : 2; }
+constexpr int pow2_at_least(int v) { return v <= 1 ? 1 : 2 * pow2_at_least((v + 1) / 2); }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -62,30 +63,29 @@ inline bool smallk_ok(int dt, int64_t D, int64_t K) {
 constexpr int64_t MAX_K = 65536;   // two radix passes of at most 8 bits
 constexpr int64_t MAX_D = 2048;
 
-// Row widths (bytes per point) the kernels handle: a power of two from 64 B
-// (16 bf16/fp16 or 16 fp32 values would be 32/64 B; D % 32 == 0 is required)
-// up to 8 KiB.
+// Row widths the kernels handle: D a multiple of 16 (rows of whole 32-byte
+// or 64-byte pieces), at most 8 KiB per row.
 inline bool row_bytes_ok(int dt, int64_t D) {
-  const int64_t rb = D * dt_bytes(dt);
-  return D % 32 == 0 && rb >= 64 && rb <= 8192 && (rb & (rb - 1)) == 0;
+  return D % 16 == 0 && D >= 16 && D * dt_bytes(dt) <= 8192;
 }
 
 // Points per assignment workgroup.  16-bit storage: 32x32x16 MFMA tiles, 4
-// waves x NSUB x 32 points (NSUB = 4 up to D = 64, 2 at 128, 1 at 256).  fp32: 16x16x4
-// MFMA tiles, 4 waves x NSUB x 16 points (NSUB = 8 up to 256-byte rows, else 4).
+// waves x NSUB x 32 points, NSUB by the D / 16 chunks a lane holds (4 up to 4
+// chunks, 2 up to 8, else 1).  fp32: 16x16x4 MFMA tiles, 4 waves x NSUB x 16
+// points (NSUB = 8 up to D = 64, else 4).
 inline int assign_nsub16(int64_t D) { return D <= 64 ? 4 : (D <= 128 ? 2 : 1); }
 inline int64_t assign_points_per_block(int dt, int64_t D) {
   if (dt != DT_F32) return 4 * 32 * assign_nsub16(D);
-  return 4 * 16 * (D * 4 / 64 <= 4 ? 8 : 4);
+  return 4 * 16 * (D / 16 <= 4 ? 8 : 4);
 }
 
-// The resident-X assignment kernels handle these row widths (bytes per point);
-// wider 16-bit rows go to the tiled kernel.
+// The resident-X assignment kernels hold a point in registers: 16-bit rows up
+// to D = 256, fp32 rows up to D = 128.  Wider 16-bit rows with D a multiple of
+// 128 go to the tiled kernel.
 inline bool assign_resident_ok(int dt, int64_t D) {
-  const int64_t rb = D * dt_bytes(dt);
-  return rb == 64 || rb == 128 || rb == 256 || rb == 512;
+  return D % 16 == 0 && D >= 16 && D <= (dt == DT_F32 ? 128 : 256);
 }
-inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D >= 512; }
+inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D > 256 && D % 128 == 0; }
 inline bool assign_ok(int dt, int64_t D) { return assign_resident_ok(dt, D) || assign_tiled(dt, D); }
 // Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
 // workgroup; its centroids are padded to whole blocks.
@@ -124,6 +124,10 @@ hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp,
                        void* chat, float* cinit, hipStream_t s);
 hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_pipe_bf16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                           int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_pipe_f16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                          int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,

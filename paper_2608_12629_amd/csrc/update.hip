@@ -244,7 +244,8 @@ __global__ __launch_bounds__(256) void bounds_kernel(const int32_t* __restrict__
 
 // ---------------------------------------------------------------------------
 // Segmented sum.  A row of D elements is RC 16-byte chunks; LPR lanes share a
-// row (CPLR chunks each) and a wave covers RPW = 64 / LPR rows per step.
+// row (CPLR chunks each, LPR * CPLR >= RC: lanes past the row's end idle) and
+// a wave covers RPW = 64 / LPR rows per step.
 template <int DT> struct Row;
 template <> struct Row<DT_F32> {
   static constexpr int per16 = 4;
@@ -281,10 +282,9 @@ template <> struct Row<DT_F16> {
 template <int DT, int LPR, int CPLR>
 __global__ __launch_bounds__(256) void segreduce_kernel(
     const uint4* __restrict__ X, const int32_t* __restrict__ perm, const int32_t* __restrict__ off,
-    int N, int K, int nred, int cr, float* __restrict__ sums, float* __restrict__ carry) {
+    int N, int K, int RC, int nred, int cr, float* __restrict__ sums, float* __restrict__ carry) {
   constexpr int E = Row<DT>::per16;
-  constexpr int RC = LPR * CPLR;
-  constexpr int D = RC * E;
+  const int D = RC * E;
   constexpr int RPW = 64 / LPR;
   constexpr int NA = CPLR * E;
   constexpr int U = 8;  // rows in flight per lane
@@ -330,7 +330,8 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
         if (pid[u] >= 0) {
           const uint4* row = xb + (size_t)pid[u] * RC + q * CPLR;
 #pragma unroll
-          for (int c = 0; c < CPLR; ++c) v[u][c] = row[c];
+          for (int c = 0; c < CPLR; ++c)
+            v[u][c] = q * CPLR + c < RC ? row[c] : make_uint4(0, 0, 0, 0);
         } else {
 #pragma unroll
           for (int c = 0; c < CPLR; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
@@ -356,6 +357,7 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
     if (r == 0) {
 #pragma unroll
       for (int c = 0; c < CPLR; ++c) {
+        if (q * CPLR + c >= RC) continue;
         float4* d4 = reinterpret_cast<float4*>(dst + (q * CPLR + c) * E);
 #pragma unroll
         for (int e = 0; e < E; e += 4)
@@ -435,11 +437,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 // floating-point atomics; every sum has a fixed order.
 template <int DT, int LPR, int CPLR>
 __global__ __launch_bounds__(1024) void smallk_partials_kernel(
-    const uint4* __restrict__ X, const int32_t* __restrict__ idx, int N, int K, int dbits, int nch,
-    float* __restrict__ partial, int32_t* __restrict__ pcount) {
+    const uint4* __restrict__ X, const int32_t* __restrict__ idx, int N, int K, int RC, int dbits,
+    int nch, float* __restrict__ partial, int32_t* __restrict__ pcount) {
   constexpr int E = Row<DT>::per16;
-  constexpr int RC = LPR * CPLR;
-  constexpr int D = RC * E;
+  const int D = RC * E;
   constexpr int RPW = 64 / LPR;
   constexpr int NA = CPLR * E;
   constexpr int U = CPLR >= 8 ? 1 : 8 / CPLR;  // rows in flight per lane (4 waves per SIMD)
@@ -522,7 +523,8 @@ __global__ __launch_bounds__(1024) void smallk_partials_kernel(
         if (jj < s1) {
           const uint4* row = xb + (size_t)plist[jj] * RC + q * CPLR;
 #pragma unroll
-          for (int c = 0; c < CPLR; ++c) v[u][c] = row[c];
+          for (int c = 0; c < CPLR; ++c)
+            v[u][c] = q * CPLR + c < RC ? row[c] : make_uint4(0, 0, 0, 0);
         } else {
 #pragma unroll
           for (int c = 0; c < CPLR; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
@@ -540,6 +542,7 @@ __global__ __launch_bounds__(1024) void smallk_partials_kernel(
     if (r == 0) {
 #pragma unroll
       for (int c = 0; c < CPLR; ++c) {
+        if (q * CPLR + c >= RC) continue;
         float4* d4 = reinterpret_cast<float4*>(pb + (size_t)kk * D + (q * CPLR + c) * E);
 #pragma unroll
         for (int e = 0; e < E; e += 4)
@@ -551,13 +554,16 @@ __global__ __launch_bounds__(1024) void smallk_partials_kernel(
   }
 }
 
-// One workgroup per cluster: the count (integer sum over chunks), then per
-// 4 dimensions the partials added in chunk order and divided by the count; an
-// empty cluster keeps its previous centroid.
+// One workgroup per cluster: the count (integer sum over chunks), then the
+// partials: each thread owns 4 consecutive dimensions, and the 256 / (D/4)
+// row slots each add every slots-th chunk in chunk order; the slot sums are
+// combined in slot order through LDS and divided by the count.  An empty
+// cluster keeps its previous centroid.
 __global__ __launch_bounds__(256) void smallk_combine_kernel(
     const float* __restrict__ partial, const int32_t* __restrict__ pcount, const float* C_prev,
     int K, int D, int nch, float* C_out, int32_t* __restrict__ counts) {
   __shared__ int wsum[4];
+  __shared__ float4 part[256];
   const int k = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   int n = 0;
   for (int c = t; c < nch; c += 256) n += pcount[((size_t)b * nch + c) * K + k];
@@ -566,44 +572,68 @@ __global__ __launch_bounds__(256) void smallk_combine_kernel(
   if (t == 0) counts[(size_t)b * K + k] = total;
   const int D4 = D / 4;
   const size_t rowoff = ((size_t)b * K + k) * D;
+  if (total == 0) {
+    for (int d = t; d < D4; d += 256)
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+    return;
+  }
   const float fn = (float)total;
-  for (int d = t; d < D4; d += 256) {
-    float4 o;
-    if (total == 0) {
-      o = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
-    } else {
-      float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int c = 0; c < nch; ++c) {
-        const float4 v = reinterpret_cast<const float4*>(
-            partial + (((size_t)b * nch + c) * K + k) * D)[d];
+  const int slots = D4 >= 256 ? 1 : 256 / D4;
+  const int slot = D4 >= 256 ? 0 : t / D4;
+  const float4* pb = reinterpret_cast<const float4*>(partial + ((size_t)b * nch * K + k) * D);
+  const size_t cstride = (size_t)K * D4;  // float4s from one chunk's row k to the next chunk's
+  for (int d0 = 0; d0 < D4; d0 += 256) {
+    const int d = d0 + (D4 >= 256 ? t : t % D4);
+    float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (slot < slots && d < D4) {
+      for (int c = slot; c < nch; c += slots) {
+        const float4 v = pb[c * cstride + d];
         sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
       }
-      o = make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
     }
-    reinterpret_cast<float4*>(C_out + rowoff)[d] = o;
+    __syncthreads();
+    part[t] = sacc;
+    __syncthreads();
+    if (slot == 0 && d < D4) {
+      for (int u = 1; u < slots; ++u) {
+        const float4 v = part[u * D4 + (t % D4)];
+        sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
+      }
+      reinterpret_cast<float4*>(C_out + rowoff)[d] =
+          make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
+    }
   }
 }
 
 template <int DT, int LPR, int CPLR>
 static void launch_smallk(const void* X, const int32_t* idx, const Workspace& w, int64_t B,
-                          int64_t N, int64_t K, int dbits, hipStream_t s) {
+                          int64_t N, int64_t K, int rc, int dbits, hipStream_t s) {
   smallk_partials_kernel<DT, LPR, CPLR><<<dim3((unsigned)w.n_sk_chunks, (unsigned)B), 1024, 0, s>>>(
-      (const uint4*)X, idx, (int)N, (int)K, dbits, (int)w.n_sk_chunks, w.partial, w.pcount);
+      (const uint4*)X, idx, (int)N, (int)K, rc, dbits, (int)w.n_sk_chunks, w.partial, w.pcount);
+}
+
+// Lanes per row (LPR) x chunks per lane (CPLR) for a row of rc 16-byte
+// chunks: the smallest power-of-two cover of rc.
+static int row_lanes(int64_t rc) {
+  int c = 2;
+  while (c < rc) c *= 2;
+  return c;  // 2 .. 512
 }
 
 template <int DT>
 static hipError_t launch_smallk_dt(const void* X, const int32_t* idx, const Workspace& w, int64_t B,
                                    int64_t N, int64_t D, int64_t K, int dbits, hipStream_t s) {
-  const int64_t rc = D * dt_bytes(DT) / 16;  // 16-byte chunks per row
-  switch (rc) {
-    case 4: launch_smallk<DT, 4, 1>(X, idx, w, B, N, K, dbits, s); break;
-    case 8: launch_smallk<DT, 8, 1>(X, idx, w, B, N, K, dbits, s); break;
-    case 16: launch_smallk<DT, 16, 1>(X, idx, w, B, N, K, dbits, s); break;
-    case 32: launch_smallk<DT, 32, 1>(X, idx, w, B, N, K, dbits, s); break;
-    case 64: launch_smallk<DT, 64, 1>(X, idx, w, B, N, K, dbits, s); break;
-    case 128: launch_smallk<DT, 64, 2>(X, idx, w, B, N, K, dbits, s); break;
-    case 256: launch_smallk<DT, 64, 4>(X, idx, w, B, N, K, dbits, s); break;
-    case 512: launch_smallk<DT, 64, 8>(X, idx, w, B, N, K, dbits, s); break;
+  const int rc = (int)(D * dt_bytes(DT) / 16);  // 16-byte chunks per row
+  switch (row_lanes(rc)) {
+    case 2: launch_smallk<DT, 2, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 4: launch_smallk<DT, 4, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 8: launch_smallk<DT, 8, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 16: launch_smallk<DT, 16, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 32: launch_smallk<DT, 32, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 64: launch_smallk<DT, 64, 1>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 128: launch_smallk<DT, 64, 2>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 256: launch_smallk<DT, 64, 4>(X, idx, w, B, N, K, rc, dbits, s); break;
+    case 512: launch_smallk<DT, 64, 8>(X, idx, w, B, N, K, rc, dbits, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -628,33 +658,28 @@ static hipError_t launch_update_smallk(const void* X, int dt, const int32_t* idx
 // ---------------------------------------------------------------------------
 template <int DT, int LPR, int CPLR>
 static void launch_segreduce(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t K,
-                             hipStream_t s) {
+                             int rc, hipStream_t s) {
   const dim3 grid((unsigned)((w.n_red_chunks + 3) / 4), (unsigned)B), block(256);
   segreduce_kernel<DT, LPR, CPLR><<<grid, block, 0, s>>>((const uint4*)X, w.perm, w.off, (int)N,
-                                                         (int)K, (int)w.n_red_chunks,
+                                                         (int)K, rc, (int)w.n_red_chunks,
                                                          (int)w.red_cr, w.sums, w.carry);
 }
 
 template <int DT>
 static hipError_t launch_segreduce_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
                                       int64_t D, int64_t K, hipStream_t s) {
-  const int64_t rc = D * dt_bytes(DT) / 16;  // 16-byte chunks per row (D % 32 == 0 => rc % 4 == 0)
-  if (rc <= 64) {
-    switch (rc) {
-      case 4: launch_segreduce<DT, 4, 1>(X, w, B, N, K, s); break;
-      case 8: launch_segreduce<DT, 8, 1>(X, w, B, N, K, s); break;
-      case 16: launch_segreduce<DT, 16, 1>(X, w, B, N, K, s); break;
-      case 32: launch_segreduce<DT, 32, 1>(X, w, B, N, K, s); break;
-      case 64: launch_segreduce<DT, 64, 1>(X, w, B, N, K, s); break;
-      default: return hipErrorInvalidValue;
-    }
-  } else {
-    switch (rc / 64) {
-      case 2: if (rc == 128) { launch_segreduce<DT, 64, 2>(X, w, B, N, K, s); break; } return hipErrorInvalidValue;
-      case 4: if (rc == 256) { launch_segreduce<DT, 64, 4>(X, w, B, N, K, s); break; } return hipErrorInvalidValue;
-      case 8: if (rc == 512) { launch_segreduce<DT, 64, 8>(X, w, B, N, K, s); break; } return hipErrorInvalidValue;
-      default: return hipErrorInvalidValue;
-    }
+  const int rc = (int)(D * dt_bytes(DT) / 16);  // 16-byte chunks per row
+  switch (row_lanes(rc)) {
+    case 2: launch_segreduce<DT, 2, 1>(X, w, B, N, K, rc, s); break;
+    case 4: launch_segreduce<DT, 4, 1>(X, w, B, N, K, rc, s); break;
+    case 8: launch_segreduce<DT, 8, 1>(X, w, B, N, K, rc, s); break;
+    case 16: launch_segreduce<DT, 16, 1>(X, w, B, N, K, rc, s); break;
+    case 32: launch_segreduce<DT, 32, 1>(X, w, B, N, K, rc, s); break;
+    case 64: launch_segreduce<DT, 64, 1>(X, w, B, N, K, rc, s); break;
+    case 128: launch_segreduce<DT, 64, 2>(X, w, B, N, K, rc, s); break;
+    case 256: launch_segreduce<DT, 64, 4>(X, w, B, N, K, rc, s); break;
+    case 512: launch_segreduce<DT, 64, 8>(X, w, B, N, K, rc, s); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

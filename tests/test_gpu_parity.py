@@ -127,6 +127,15 @@ SHAPES = [
     (1, 300, 64, 300, "bf16"),        # K = N
     (2, 6000, 128, 128, "bf16"),      # per-chunk update at K * D = 16384, ragged chunk
     (1, 10000, 32, 512, "f32"),       # per-chunk update, fp32, 9-bit cluster ids
+    (1, 3000, 16, 10, "bf16"),        # D = 16: one chunk per lane
+    (1, 3000, 48, 37, "f16"),         # D = 48: padded LDS rows, masked row lanes
+    (2, 1500, 96, 50, "bf16"),        # D = 96
+    (1, 2000, 160, 70, "bf16"),       # D = 160: one column tile per wave, padded rows
+    (1, 2000, 208, 33, "f16"),        # D = 208
+    (1, 3000, 48, 20, "f32"),         # fp32 D = 48: padded LDS rows
+    (1, 3000, 112, 40, "f32"),        # fp32 D = 112
+    (1, 3000, 80, 300, "f32"),        # fp32 D = 80, sorted update with masked row lanes
+    (1, 1500, 384, 300, "bf16"),      # tiled kernel, D = 384
     (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
     (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
