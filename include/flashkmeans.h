@@ -32,7 +32,7 @@
  *   a rejected call returns a negative status and has no effect.
  *   FKM_ERR_UNSUPPORTED means valid but outside what this build implements:
  *   not gfx950; D not a multiple of 16; D > 2048; bf16/fp16 D above 256 and
- *   not a multiple of 128; fp32 D > 128; K > 65536; N > 2^31-1; B > 65535.
+ *   not a multiple of 32; fp32 D > 256; K > 65536; N > 2^31-1; B > 65535.
  *   FKM_ERR_HIP reports a failed HIP call or launch.  No C++ exception
  *   crosses this boundary.
  */

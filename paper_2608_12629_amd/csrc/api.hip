@@ -49,7 +49,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   w.partial = (float*)take(sk ? (size_t)(B * w.n_sk_chunks * K * D) * 4 : 0);
   w.pcount = (int32_t*)take(sk ? (size_t)(B * w.n_sk_chunks * K) * 4 : 0);
   const bool tiled = assign_tiled(dt, D);
-  w.keys = (uint64_t*)take(tiled ? (size_t)(B * N) * 8 : 0);
+  w.keys = (uint64_t*)take(tiled ? (size_t)(B * N + 1) * 8 + TILED_ZERO_BYTES : 0);
   w.xnorm = (float*)take(tiled ? (size_t)(B * N) * 4 : 0);
   w.total = o;
   return w;

@@ -250,7 +250,7 @@ hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp,
 template <int DT, int CPL>
 static hipError_t launch_resident(const void* X, const Workspace& w, int64_t B, int64_t N,
                                   int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
-  constexpr int NSUB = CPL <= 4 ? 8 : 4;
+  constexpr int NSUB = CPL <= 4 ? 8 : (CPL <= 8 ? 4 : 2);  // must agree with assign_nsub32
   const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
   assign_resident_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
       (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)K, (int)w.Kp, idx, min_dist,
@@ -272,6 +272,14 @@ static hipError_t launch_resident_dt(const void* X, const Workspace& w, int64_t 
     case 6: return launch_resident<DT, 6>(X, w, B, N, K, idx, min_dist, s);
     case 7: return launch_resident<DT, 7>(X, w, B, N, K, idx, min_dist, s);
     case 8: return launch_resident<DT, 8>(X, w, B, N, K, idx, min_dist, s);
+    case 9: return launch_resident<DT, 9>(X, w, B, N, K, idx, min_dist, s);
+    case 10: return launch_resident<DT, 10>(X, w, B, N, K, idx, min_dist, s);
+    case 11: return launch_resident<DT, 11>(X, w, B, N, K, idx, min_dist, s);
+    case 12: return launch_resident<DT, 12>(X, w, B, N, K, idx, min_dist, s);
+    case 13: return launch_resident<DT, 13>(X, w, B, N, K, idx, min_dist, s);
+    case 14: return launch_resident<DT, 14>(X, w, B, N, K, idx, min_dist, s);
+    case 15: return launch_resident<DT, 15>(X, w, B, N, K, idx, min_dist, s);
+    case 16: return launch_resident<DT, 16>(X, w, B, N, K, idx, min_dist, s);
     default: return hipErrorInvalidValue;
   }
 }

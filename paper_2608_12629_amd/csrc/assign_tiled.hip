@@ -1,5 +1,5 @@
 // assign_tiled.hip -- the assignment step for wide rows (16-bit points with
-// D >= 512), where a point no longer fits in registers.
+// D > 256, a multiple of 32), where a point no longer fits in registers.
 //
 // The distance contraction is tiled like a GEMM.  A workgroup owns 256 points
 // and up to TILED_CBG consecutive 256-centroid blocks; its four waves split
@@ -35,6 +35,12 @@
 // depends only on the point block, so every workgroup of a point block uses
 // the same Q, and the decode pass recomputes it the same way.
 //
+// Blocks of D.  A block of centroids takes nds = D / 32 stages, padded to a
+// multiple of four (the buffer rotation).  A padding stage reloads the block's
+// last point stage and loads its centroid chunks from a zeroed scratch area,
+// so every stage issues the same loads and runs the same code: its MFMAs add
+// a finite x times zero, which is exactly zero.
+//
 // Block order is XCD-aware: workgroup ids go round-robin over the 8 XCDs, and
 // each XCD walks super-tiles of 8 point blocks x all centroid groups (point
 // block fastest), so the workgroups resident on an XCD share both operands
@@ -57,6 +63,7 @@ constexpr int LC = BC * CPS / 256;       // centroid chunks per thread per stage
 constexpr int LOADS = LX + LC + 1;       // loads per thread per stage (+ one score)
 static_assert(BP == 256 && BC == 256, "2 x 2 waves of 128 x 128");
 static_assert(2 * LOADS <= 63, "vmcnt counts at most 63 loads");
+static_assert(CB <= TILED_ZERO_BYTES, "a padding stage's centroid chunks fit the zero area");
 
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
@@ -97,18 +104,22 @@ struct TiledCtx {
   const char* X;       // the workgroup's first point row
   const char* chat;    // this instance's rounded centroids
   const float* cinit;  // this instance's -|c^|^2/2
+  const char* zero;    // CB zeroed bytes: the centroid chunks of a padding stage
   uint32_t xoff;       // lane byte offset of its first point chunk (row clamped to the last point)
   uint32_t coff;       // lane byte offset of its first centroid chunk
   uint32_t rows64;     // bytes of 64 rows
   int last;            // last valid row of the point block
-  int nds, cb0, RC, tid, S, loff0, loff1, wp, wc;
+  int nds;             // stages of 32 dimensions per block (D / 32)
+  int ndsv;            // stages per block, padded to a multiple of 4
+  int cb0, RC, tid, S, loff0, loff1, wp, wc;
 };
 
-// Stage s = (block s / nds, dimensions 32 (s % nds) ..): start its loads into buf.
+// Stage s = (block s / ndsv, dimensions 32 (s % ndsv) ..): start its loads into buf.
 // Load u of a thread covers slot tid + 256 u: row tid / 4 + 64 u, chunk
 // (tid % 4) ^ swz(row) (swz has period 16, so the chunk order repeats).
 __device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf) {
-  const int g = s / c.nds, ds = s % c.nds;
+  const int g = s / c.ndsv, dv = s % c.ndsv, ds = min(dv, c.nds - 1);
+  const bool pad = dv >= c.nds;
   const int wave = __builtin_amdgcn_readfirstlane(c.tid >> 6);
   const char* xb = c.X + ds * CPS * 16;
 #pragma unroll
@@ -123,9 +134,11 @@ __device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf)
   const int krow = (c.cb0 + g) * BC;
   const char* cbp = c.chat + ((size_t)krow * c.RC + ds * CPS) * 16;
 #pragma unroll
-  for (int u = 0; u < LC; ++u)
-    __builtin_amdgcn_global_load_lds((global_void*)(cbp + c.coff + u * c.rows64),
+  for (int u = 0; u < LC; ++u) {
+    const char* src = pad ? c.zero + (u * 256 + c.tid) * 16 : cbp + c.coff + u * c.rows64;
+    __builtin_amdgcn_global_load_lds((global_void*)src,
                                      (lds_void*)(buf + XB + (u * 256 + wave * 64) * 16), 16, 0, 0);
+  }
   // the block's scores ride with every stage, so every stage issues LOADS loads
   __builtin_amdgcn_global_load_lds((global_void*)(c.cinit + krow + c.tid),
                                    (lds_void*)(buf + XB + CB + wave * 256), 4, 0, 0);
@@ -230,8 +243,8 @@ __device__ __forceinline__ void tiled_epilogue(const f32x16 (&acc)[4][4], float 
 template <int DT>
 __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
-    const float* __restrict__ xnorm, int N, int D, int Kp, int npb, int ncbg,
-    uint64_t* __restrict__ keys) {
+    const float* __restrict__ xnorm, const uint4* __restrict__ zero, int N, int D, int Kp, int npb,
+    int ncbg, uint64_t* __restrict__ keys) {
   __shared__ __attribute__((aligned(16))) char buf0[STAGE];
   __shared__ __attribute__((aligned(16))) char buf1[STAGE];
   __shared__ __attribute__((aligned(16))) char buf2[STAGE];
@@ -250,6 +263,7 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   const int p0 = pb * BP;
   const int RC = D / 8;  // 16-byte chunks per row
   const int nds = D / DC;
+  const int ndsv = (nds + 3) / 4 * 4;
   const int cb0 = cbg * TILED_CBG;
   const int ncbw = min(TILED_CBG, Kp / BC - cb0);  // centroid blocks of this workgroup
 
@@ -257,15 +271,17 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   c.X = reinterpret_cast<const char*>(X + ((size_t)b * N + p0) * RC);
   c.chat = reinterpret_cast<const char*>(chat + (size_t)b * Kp * RC);
   c.cinit = cinit + (size_t)b * Kp;
+  c.zero = reinterpret_cast<const char*>(zero);
   c.last = min(BP, N - p0) - 1;
   c.xoff = (uint32_t)((min(tid >> 2, c.last) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
   c.coff = (uint32_t)(((tid >> 2) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
   c.rows64 = (uint32_t)(64 * RC * 16);
   c.nds = nds;
+  c.ndsv = ndsv;
   c.cb0 = cb0;
   c.RC = RC;
   c.tid = tid;
-  c.S = ncbw * nds;
+  c.S = ncbw * ndsv;
   // fragment reads: lane 32 h + n takes row (tile base + n), chunk 2 ks + h
   c.loff0 = n * 64 + ((0 + h) ^ swz(n)) * 16;
   c.loff1 = n * 64 + ((2 + h) ^ swz(n)) * 16;
@@ -299,10 +315,10 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   }
   TiledFrag f0, f1;
   tiled_read(f0, buf0, c.loff0, wp, wc);
-  const int nq = nds / 4;  // nds % 4 == 0: every block starts in buffer 0
+  const int nq = ndsv / 4;  // every block starts in buffer 0
   for (int g = 0; g < ncbw; ++g) {
     tiled_init(acc, buf0, wc, h, Q);
-    const int s0 = g * nds;
+    const int s0 = g * ndsv;
     const int full = g == ncbw - 1 ? nq - 1 : nq;  // quads with no stage past the end
     for (int q = 0; q < full; ++q)
       tiled_quad<DT, false>(c, s0 + 4 * q, buf0, buf1, buf2, buf3, acc, f0, f1);
@@ -413,9 +429,12 @@ __global__ __launch_bounds__(256) void decode_keys_kernel(const uint64_t* __rest
 
 hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s) {
-  if (D % (4 * DC) != 0 || w.Kp % BC != 0) return hipErrorInvalidValue;
+  if (D % DC != 0 || w.Kp % BC != 0) return hipErrorInvalidValue;
   const int64_t nk = B * N;
-  fill_keys_kernel<<<dim3((unsigned)((nk + 255) / 256)), 256, 0, s>>>(w.keys, nk);
+  // the keys, then TILED_ZERO_BYTES of zeros for padding stages (16-byte aligned)
+  const int64_t nz = (nk + 1) & ~int64_t(1);
+  const int64_t nfill = nz + TILED_ZERO_BYTES / 8;
+  fill_keys_kernel<<<dim3((unsigned)((nfill + 255) / 256)), 256, 0, s>>>(w.keys, nfill);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int RC = (int)(D / 8);
@@ -433,12 +452,12 @@ hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_
   const dim3 grid((unsigned)(npb64 * ncbg), (unsigned)B);
   if (dt == DT_BF16)
     assign_tiled_kernel<DT_BF16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
-                                                      w.cinit, w.xnorm, (int)N, (int)D, (int)w.Kp,
-                                                      npb, ncbg, w.keys);
+                                                      w.cinit, w.xnorm, (const uint4*)(w.keys + nz),
+                                                      (int)N, (int)D, (int)w.Kp, npb, ncbg, w.keys);
   else
     assign_tiled_kernel<DT_F16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
-                                                     w.cinit, w.xnorm, (int)N, (int)D, (int)w.Kp,
-                                                     npb, ncbg, w.keys);
+                                                     w.cinit, w.xnorm, (const uint4*)(w.keys + nz),
+                                                     (int)N, (int)D, (int)w.Kp, npb, ncbg, w.keys);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   decode_keys_kernel<<<dim3((unsigned)w.n_assign_blocks, (unsigned)B), 256, 0, s>>>(
       w.keys, w.xnorm, (int)N, idx, min_dist, w.objpart);

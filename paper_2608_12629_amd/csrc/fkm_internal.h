@@ -72,24 +72,23 @@ inline bool row_bytes_ok(int dt, int64_t D) {
 // Points per assignment workgroup.  16-bit storage: 32x32x16 MFMA tiles, 4
 // waves x NSUB x 32 points, NSUB by the D / 16 chunks a lane holds (4 up to 4
 // chunks, 2 up to 8, else 1).  fp32: 16x16x4 MFMA tiles, 4 waves x NSUB x 16
-// points (NSUB = 8 up to D = 64, else 4).
+// points (NSUB = 8 up to D = 64, 4 up to 128, else 2).
 inline int assign_nsub16(int64_t D) { return D <= 64 ? 4 : (D <= 128 ? 2 : 1); }
+inline int assign_nsub32(int64_t D) { return D <= 64 ? 8 : (D <= 128 ? 4 : 2); }
 inline int64_t assign_points_per_block(int dt, int64_t D) {
   if (dt != DT_F32) return 4 * 32 * assign_nsub16(D);
-  return 4 * 16 * (D / 16 <= 4 ? 8 : 4);
+  return 4 * 16 * assign_nsub32(D);
 }
 
-// The resident-X assignment kernels hold a point in registers: 16-bit rows up
-// to D = 256, fp32 rows up to D = 128.  Wider 16-bit rows with D a multiple of
-// 128 go to the tiled kernel.
-inline bool assign_resident_ok(int dt, int64_t D) {
-  return D % 16 == 0 && D >= 16 && D <= (dt == DT_F32 ? 128 : 256);
-}
-inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D > 256 && D % 128 == 0; }
+// The resident-X assignment kernels hold a point in registers: rows up to
+// D = 256.  Wider 16-bit rows with D a multiple of 32 go to the tiled kernel.
+inline bool assign_resident_ok(int dt, int64_t D) { return D % 16 == 0 && D >= 16 && D <= 256; }
+inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D > 256 && D % 32 == 0; }
 inline bool assign_ok(int dt, int64_t D) { return assign_resident_ok(dt, D) || assign_tiled(dt, D); }
 // Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
 // workgroup; its centroids are padded to whole blocks.
 constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 4;
+constexpr int64_t TILED_ZERO_BYTES = 16384;  // zeros after the keys (padding stages)
 inline int64_t kpad_for(int dt, int64_t D, int64_t K) {
   return assign_tiled(dt, D) ? (K + TILED_BC - 1) / TILED_BC * TILED_BC : kpad(K);
 }
@@ -111,7 +110,7 @@ struct Workspace {
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
   float* partial;  // [B,n_sk_chunks,K,D] per-chunk cluster sums (small-K update only)
   int32_t* pcount; // [B,n_sk_chunks,K] per-chunk cluster counts (small-K update only)
-  uint64_t* keys;  // [B,N] best (score, index) of each point (tiled assignment only)
+  uint64_t* keys;  // [B,N] best (score, index) of each point, then TILED_ZERO_BYTES of zeros (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
   int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr, n_sk_chunks;
   size_t total;

@@ -71,9 +71,9 @@ def test_workspace_bytes(lib):
     # rejected shapes report 0
     assert ws(0, 10, 64, 4) == 0 and ws(1, 0, 64, 4) == 0 and ws(1, 10, 64, 0) == 0
     assert ws(1, 10, 40, 4) == 0            # D not a multiple of 16
-    for D in (16, 48, 96, 160, 208, 256, 384, 640, 2048):
+    for D in (16, 48, 96, 160, 208, 256, 288, 384, 640, 992, 2048):
         assert ws(1, 1000, D, 10) > 0, D    # 16-bit shapes in the domain
-    for D in (16, 48, 80, 112, 128):
+    for D in (16, 48, 80, 112, 128, 144, 256):
         assert ws(1, 1000, D, 10, F32) > 0, D
     assert ws(1, 10, 64, 70000) == 0        # K above the sort limit
     assert ws(1, 10, 64, 4, 7) == 0         # unknown dtype
@@ -109,8 +109,8 @@ def test_rejections_before_any_device_call(lib, call):
     assert call(lib, D=0) == EINVAL
     assert call(lib, D=40) == EUNSUP          # not a multiple of 16
     assert call(lib, D=4096) == EUNSUP
-    assert call(lib, D=272) == EUNSUP         # 16-bit rows past 256 must be multiples of 128
-    assert call(lib, dt=F32, D=144) == EUNSUP  # fp32 rows up to 128
+    assert call(lib, D=272) == EUNSUP         # 16-bit rows past 256 must be multiples of 32
+    assert call(lib, dt=F32, D=272) == EUNSUP  # fp32 rows up to 256
     assert call(lib, K=70000) == EUNSUP
     assert call(lib, N=1 << 31) == EUNSUP
     assert call(lib, ws=None) == EWS

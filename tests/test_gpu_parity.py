@@ -135,7 +135,12 @@ SHAPES = [
     (1, 3000, 48, 20, "f32"),         # fp32 D = 48: padded LDS rows
     (1, 3000, 112, 40, "f32"),        # fp32 D = 112
     (1, 3000, 80, 300, "f32"),        # fp32 D = 80, sorted update with masked row lanes
+    (1, 3000, 144, 30, "f32"),        # fp32 D = 144: two column tiles per wave
+    (1, 2000, 256, 50, "f32"),        # fp32 D = 256
     (1, 1500, 384, 300, "bf16"),      # tiled kernel, D = 384
+    (1, 1200, 288, 90, "f16"),        # tiled, D = 288: 9 stages + 3 padding stages per block
+    (2, 900, 416, 257, "bf16"),       # tiled, D = 416: 13 + 3
+    (1, 700, 992, 40, "bf16"),        # tiled, D = 992: 31 + 1
     (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
     (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
