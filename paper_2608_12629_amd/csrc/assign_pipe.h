@@ -50,7 +50,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 // Per-lane offsets, fixed for the whole kernel.
 template <int CPL, int LOADS>
 struct PipeOffsets {
-  int src[LOADS];    // chunk of a stage that lands in LDS slot tid + u * 256 (-1: a padding slot)
+  int src[LOADS];    // chunk of a stage that lands in LDS slot tid + u * 256
   int a[CPL];        // byte offset of chunk h * CPL + c of centroid row n of tile 0
   int n_store;       // byte offset of the score slot written by this thread
   int n_read;        // byte offset of the first score read by this lane (rows 4 h .. 4 h + 3)
@@ -75,7 +75,9 @@ __device__ __forceinline__ void pipe_offsets(PipeOffsets<CPL, LOADS>& o, int tid
   for (int u = 0; u < LOADS; ++u) {  // slot s holds row s / RCP, chunk (s % RCP) ^ (row & SWZ)
     const int sl = tid + u * ASSIGN_THREADS;
     const int r = sl / L::RCP, c = (sl % L::RCP) ^ (r & L::SWZ);
-    o.src[u] = c < L::RC ? r * L::RC + c : -1;
+    // a padding slot (c >= RC) is never read: it loads the row's first chunk,
+    // so every lane loads and the stage code has no branch
+    o.src[u] = r * L::RC + (c < L::RC ? c : 0);
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) o.a[c] = (n * L::RCP + ((h * CPL + c) ^ (n & L::SWZ))) * 16;
@@ -100,10 +102,9 @@ __device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
   for (int u = 0; u < LOADS; ++u)
-    if (L::RC == L::RCP || o.src[u] >= 0)  // padding slots are never read
-      __builtin_amdgcn_global_load_lds((global_void*)(src + o.src[u]),
-                                       (lds_void*)(buf + (u * ASSIGN_THREADS + wave * 64) * 16), 16,
-                                       0, 0);
+    __builtin_amdgcn_global_load_lds((global_void*)(src + o.src[u]),
+                                     (lds_void*)(buf + (u * ASSIGN_THREADS + wave * 64) * 16), 16, 0,
+                                     0);
   return cinit[st * L::TCS + (tid & (L::TCS - 1))];
 }
 
