@@ -26,7 +26,7 @@ PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16/fp16 MFMA (no sparsity)
 PEAK_F32_TFLOPS = 157.3            # MI355X fp32 MFMA
 PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "assign_traffic.json")
-ASSIGN_SRC = os.path.join(ROOT, "paper_2608_12629_amd", "csrc", "assign.hip")
+ASSIGN_SRC = os.path.join(ROOT, "paper_2608_12629_amd", "csrc", "assign_pipe.h")
 
 
 def log(*a):
