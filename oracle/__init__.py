@@ -6,7 +6,7 @@ with the HIP library.
 
 ``kmeans_oracle.c`` holds the arithmetic (assignment by direct squared
 distances with a lowest-index arg-min, per-cluster means with empty clusters
-kept, the objective).  This module only marshals numpy arrays into it.  Points
+kept, the objective, and the k nearest rows of a KNN search).  This module only marshals numpy arrays into it.  Points
 are passed as stored: float32 arrays, or uint16 arrays of bf16/fp16 bits.
 ``oracle/exact.py`` has an exact-rational version for tiny inputs.
 """
@@ -38,7 +38,9 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.oracle_assign.argtypes = [vp, i32, dp, i64, i64, i64, i64, vp, dp, dp]
     lib.oracle_update.argtypes = [vp, i32, vp, dp, i64, i64, i64, i64, dp, vp]
     lib.oracle_lloyd.argtypes = [vp, i32, dp, i64, i64, i64, i64, i32, dp, vp, dp, vp, dp]
-    for f in (lib.oracle_widen, lib.oracle_assign, lib.oracle_update, lib.oracle_lloyd):
+    lib.oracle_knn.argtypes = [vp, vp, i32, i64, i64, i64, i64, i64, vp, dp, dp]
+    for f in (lib.oracle_widen, lib.oracle_assign, lib.oracle_update, lib.oracle_lloyd,
+              lib.oracle_knn):
         f.restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -122,6 +124,24 @@ class Oracle:
         if rc:
             raise ValueError(f"oracle_lloyd failed ({rc})")
         return C_out, idx, md, counts, obj
+
+    def knn(self, Q: np.ndarray, R: np.ndarray, dtype: str, k: int):
+        """KNN search: returns idx [B,M,k] int32, dist [B,M,k] fp64 (increasing,
+        ties to the lowest index) and next_dist [B,M] (the (k+1)-th distance)."""
+        Q = self._points(Q, dtype)
+        R = self._points(R, dtype)
+        B, M, D = Q.shape
+        if R.shape[0] != B or R.shape[2] != D:
+            raise ValueError("queries and database must share B and D")
+        N = R.shape[1]
+        idx = np.empty((B, M, k), np.int32)
+        dist = np.empty((B, M, k), np.float64)
+        nxt = np.empty((B, M), np.float64)
+        rc = self.lib.oracle_knn(self._ptr(Q), self._ptr(R), _DT[dtype], B, M, N, D, k,
+                                 self._ptr(idx), self._ptr(dist), self._ptr(nxt))
+        if rc:
+            raise ValueError(f"oracle_knn failed ({rc})")
+        return idx, dist, nxt
 
 
 _default: Optional[Oracle] = None

@@ -6,7 +6,7 @@ agree bit for bit, and for general inputs up to fp64 rounding.
 
 Also enumerates every labelling of a tiny point set to find the global minimum
 of the k-means objective, which Lloyd's local search can only approach from
-above.
+above, and sorts exact distances for KNN search.
 """
 from __future__ import annotations
 
@@ -78,3 +78,16 @@ def partition_cost(X: List[Vec], labels: Sequence[int], K: int) -> Fraction:
 def global_minimum(X: List[Vec], K: int) -> Fraction:
     """Minimum objective over all K^N labellings (tiny N only)."""
     return min(partition_cost(X, lab, K) for lab in itertools.product(range(K), repeat=len(X)))
+
+
+def knn(Q: List[Vec], R: List[Vec], k: int):
+    """k nearest rows of R for each query: (indices, distances, next distance),
+    ordered by (distance, index); the next distance is None when k == len(R)."""
+    out_i, out_d, out_n = [], [], []
+    for q in Q:
+        d = [sqdist(q, r) for r in R]
+        order = sorted(range(len(R)), key=lambda j: (d[j], j))
+        out_i.append(order[:k])
+        out_d.append([d[j] for j in order[:k]])
+        out_n.append(d[order[k]] if k < len(R) else None)
+    return out_i, out_d, out_n

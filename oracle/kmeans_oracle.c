@@ -27,6 +27,14 @@
  * Readings where the paper is silent: ties go to the lowest index; an empty
  * cluster keeps its previous centroid; J_t is the objective of the assignment
  * made under C_t, before that iteration's update.
+ *
+ * KNN search (the same distance with a top-k instead of an arg-min; the paper
+ * lists KNN build and search beside KMeans in Section 6 and reports recall
+ * 1.0): for query q and database rows r_j,
+ *
+ *   e_j       = sum_l (q_l - r_jl)^2             direct form, l ascending, fp64
+ *   nbr       = the k smallest e_j in increasing order, ties -> lowest j
+ *   next_dist = the (k+1)-th smallest e_j (+inf when k == N)
  */
 #include <math.h>
 #include <stdint.h>
@@ -178,5 +186,70 @@ int oracle_lloyd(const void* X, int dtype, const double* C0, int64_t B, int64_t 
         memcpy(C, C_out, (size_t)(B * K * D) * sizeof(double));
     }
     free(C);
+    return err;
+}
+
+/*
+ * KNN search for B instances: queries Q [B,M,D] and database R [B,N,D], both
+ * stored in `dtype`.  nbr_idx / nbr_dist [B,M,k]; next_dist [B,M] may be NULL.
+ * Each query keeps its k + 1 smallest distances by insertion into a list
+ * ordered by (distance, index).
+ */
+int oracle_knn(const void* Q, const void* R, int dtype, int64_t B, int64_t M, int64_t N,
+               int64_t D, int64_t k, int32_t* nbr_idx, double* nbr_dist, double* next_dist) {
+    if (!Q || !R || !nbr_idx || !nbr_dist || !dtype_ok(dtype) || B < 1 || M < 0 || N < 1 ||
+        D < 1 || k < 1 || k > N)
+        return ORC_EINVAL;
+    double* rw = (double*)malloc((size_t)(N * D) * sizeof(double));
+    if (!rw) return ORC_ENOMEM;
+    int err = ORC_OK;
+    for (int64_t b = 0; b < B && err == ORC_OK; ++b) {
+        for (int64_t j = 0; j < N * D; ++j) rw[j] = widen_one(R, dtype, b * N * D + j);
+#pragma omp parallel
+        {
+            double* q = (double*)malloc((size_t)D * sizeof(double));
+            double* ld = (double*)malloc((size_t)(k + 1) * sizeof(double));
+            int64_t* li = (int64_t*)malloc((size_t)(k + 1) * sizeof(int64_t));
+            if (!q || !ld || !li) {
+#pragma omp atomic write
+                err = ORC_ENOMEM;
+            }
+#pragma omp for schedule(static)
+            for (int64_t i = 0; i < M; ++i) {
+                if (!q || !ld || !li) continue;
+                const int64_t row = b * M + i;
+                for (int64_t l = 0; l < D; ++l) q[l] = widen_one(Q, dtype, row * D + l);
+                int64_t n = 0;  /* entries in the list, at most k + 1 */
+                for (int64_t j = 0; j < N; ++j) {
+                    const double* r = rw + j * D;
+                    double e = 0.0;
+                    for (int64_t l = 0; l < D; ++l) {
+                        const double t = q[l] - r[l];
+                        e += t * t;
+                    }
+                    /* j ascending: an equal distance goes after the entries already there */
+                    if (n == k + 1 && !(e < ld[k])) continue;
+                    int64_t pos = n < k + 1 ? n : k;
+                    while (pos > 0 && e < ld[pos - 1]) {
+                        ld[pos] = ld[pos - 1];
+                        li[pos] = li[pos - 1];
+                        --pos;
+                    }
+                    ld[pos] = e;
+                    li[pos] = j;
+                    if (n < k + 1) ++n;
+                }
+                for (int64_t t = 0; t < k; ++t) {
+                    nbr_idx[row * k + t] = (int32_t)li[t];
+                    nbr_dist[row * k + t] = ld[t];
+                }
+                if (next_dist) next_dist[row] = n > k ? ld[k] : INFINITY;
+            }
+            free(q);
+            free(ld);
+            free(li);
+        }
+    }
+    free(rw);
     return err;
 }

@@ -7,7 +7,9 @@ fixes: exact rational arithmetic, a hand-worked example, library routines
 and torch's bfloat16 conversions), closed forms, invariants and brute-force
 enumeration.  ``test_oracle_pins.py`` runs them against the real oracle;
 ``test_oracle_mutants.py`` runs them against copies with planted mistakes and
-requires every mistake to be caught.
+requires every mistake to be caught.  ``KNN_PINS`` do the same for the KNN
+search (exact sorting, scipy's k-d tree, scikit-learn's brute-force
+neighbours, torch's cdist, the assignment step as k = 1).
 """
 from __future__ import annotations
 
@@ -357,3 +359,99 @@ FAST_PINS = [pin_widen_bf16, pin_widen_f16, pin_exact_dyadic, pin_exact_general,
              pin_duplicate_centroids, pin_1d_midpoints, pin_empty_cluster_kept,
              pin_batched_independent, pin_mass_conservation, pin_fixed_point, pin_blob_recovery,
              pin_global_minimum]
+
+
+# ------------------------------------------------------------------ KNN search
+def pin_knn_exact_dyadic(o, seed=21):
+    """Dyadic inputs on a coarse grid (many equal distances): the oracle's k nearest
+    rows, their order, distances and the next distance equal exact sorting."""
+    rng = np.random.default_rng(seed)
+    for trial in range(12):
+        M = int(rng.integers(1, 7))
+        N = int(rng.integers(1, 12))
+        D = int(rng.integers(1, 4))
+        k = int(rng.integers(1, N + 1))
+        Q = _dyadic(rng, (M, D), den=2, span=3)
+        R = _dyadic(rng, (N, D), den=2, span=3)
+        idx, dist, nxt = o.knn(_f32(Q), _f32(R), "f32", k)
+        ei, ed, en = exact.knn(exact.to_frac(Q), exact.to_frac(R), k)
+        for i in range(M):
+            assert idx[0, i].tolist() == ei[i]
+            assert [Fraction(v) for v in dist[0, i]] == ed[i]
+            assert (np.isinf(nxt[0, i]) if en[i] is None else Fraction(nxt[0, i]) == en[i])
+
+
+def pin_knn_ckdtree(o, seed=22):
+    """scipy's k-d tree (exact search) on continuous data: same rows, same order."""
+    from scipy.spatial import cKDTree
+    rng = np.random.default_rng(seed)
+    R = _f32(rng.standard_normal((700, 6)))
+    Q = _f32(rng.standard_normal((90, 6)))
+    dd, ii = cKDTree(R.astype(np.float64)).query(Q.astype(np.float64), k=9)
+    idx, dist, nxt = o.knn(Q, R, "f32", 9)
+    assert np.array_equal(idx[0], ii)
+    assert np.allclose(dist[0], dd ** 2, rtol=1e-12, atol=1e-12)
+    d10, _ = cKDTree(R.astype(np.float64)).query(Q.astype(np.float64), k=10)
+    assert np.allclose(nxt[0], d10[:, 9] ** 2, rtol=1e-12, atol=1e-12)
+
+
+def pin_knn_sklearn_bf16(o, seed=23):
+    """bf16 storage: scikit-learn's brute-force neighbours on the widened values."""
+    from sklearn.neighbors import NearestNeighbors
+    rng = np.random.default_rng(seed)
+    Rb = _bits(rng.uniform(-1, 1, (400, 12)), "bf16")
+    Qb = _bits(rng.uniform(-1, 1, (60, 12)), "bf16")
+    R64 = torch.from_numpy(Rb.view(np.int16)).view(torch.bfloat16).double().numpy()
+    Q64 = torch.from_numpy(Qb.view(np.int16)).view(torch.bfloat16).double().numpy()
+    nn = NearestNeighbors(n_neighbors=5, algorithm="brute").fit(R64)
+    dd, ii = nn.kneighbors(Q64)
+    idx, dist, _ = o.knn(Qb, Rb, "bf16", 5)
+    # rows within a distance tie may come in another order from the library
+    clear = np.all(np.diff(dd ** 2, axis=1) > 1e-12, axis=1)
+    assert np.array_equal(idx[0][clear], ii[clear])
+    assert np.allclose(dist[0], dd ** 2, rtol=1e-9, atol=1e-12)
+
+
+def pin_knn_self_and_full_order(o, seed=24):
+    """Queries equal to database rows find themselves at distance 0; k = N lists
+    every row, by torch.cdist distance (fp64, direct form), stably."""
+    rng = np.random.default_rng(seed)
+    R = _f32(rng.standard_normal((50, 5)))
+    idx, dist, nxt = o.knn(R, R, "f32", 3)
+    assert np.array_equal(idx[0, :, 0], np.arange(50))
+    assert np.all(dist[0, :, 0] == 0.0)
+    Q = _f32(rng.standard_normal((7, 5)))
+    idx, dist, nxt = o.knn(Q, R, "f32", 50)
+    d = torch.cdist(torch.from_numpy(Q.astype(np.float64)), torch.from_numpy(R.astype(np.float64)),
+                    compute_mode="donot_use_mm_for_euclid_dist").numpy() ** 2
+    ref = np.argsort(d, axis=1, kind="stable")
+    assert np.array_equal(idx[0], ref)
+    assert np.all(np.isinf(nxt[0]))
+
+
+def pin_knn_k1_is_assignment(o, seed=25):
+    """k = 1 is the assignment step with the database as the centroids."""
+    rng = np.random.default_rng(seed)
+    R = _dyadic(rng, (30, 3), den=2, span=2)       # coarse: ties occur
+    Q = _dyadic(rng, (200, 3), den=2, span=2)
+    idx, dist, nxt = o.knn(_f32(Q), _f32(R), "f32", 1)
+    a_idx, a_md, a_gap = o.assign(_f32(Q), "f32", R.astype(np.float64))
+    assert np.array_equal(idx[0, :, 0], a_idx[0])
+    assert np.array_equal(dist[0, :, 0], a_md[0])
+    assert np.array_equal(nxt[0] - dist[0, :, 0], a_gap[0])
+
+
+def pin_knn_batched(o, seed=26):
+    """B instances are independent: stacked results equal per-instance results."""
+    rng = np.random.default_rng(seed)
+    Q = _f32(rng.standard_normal((3, 20, 4)))
+    R = _f32(rng.standard_normal((3, 35, 4)))
+    idx, dist, nxt = o.knn(Q, R, "f32", 4)
+    for b in range(3):
+        i1, d1, n1 = o.knn(Q[b], R[b], "f32", 4)
+        assert np.array_equal(idx[b], i1[0]) and np.array_equal(dist[b], d1[0])
+        assert np.array_equal(nxt[b], n1[0])
+
+
+KNN_PINS = [pin_knn_exact_dyadic, pin_knn_ckdtree, pin_knn_sklearn_bf16, pin_knn_self_and_full_order,
+            pin_knn_k1_is_assignment, pin_knn_batched]

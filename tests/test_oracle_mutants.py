@@ -34,6 +34,20 @@ MUTANTS = {
 }
 
 
+# planted mistakes in the KNN search, each caught by the KNN pins
+KNN_MUTANTS = {
+    "knn_tie_to_later": ("while (pos > 0 && e < ld[pos - 1]) {", "while (pos > 0 && e <= ld[pos - 1]) {"),
+    "knn_sign_flip": ("const double t = q[l] - r[l];", "const double t = q[l] + r[l];"),
+    "knn_keeps_k_only": ("int64_t n = 0;  /* entries in the list, at most k + 1 */",
+                         "int64_t n = 1;  /* entries in the list, at most k + 1 */"),
+    "knn_next_is_kth": ("if (next_dist) next_dist[row] = n > k ? ld[k] : INFINITY;",
+                        "if (next_dist) next_dist[row] = n > k ? ld[k - 1] : INFINITY;"),
+    "knn_instance_stride": ("rw[j] = widen_one(R, dtype, b * N * D + j);", "rw[j] = widen_one(R, dtype, j);"),
+    "knn_drops_last_dim": ("for (int64_t l = 0; l < D; ++l) {\n                        const double t",
+                           "for (int64_t l = 0; l + 1 < D; ++l) {\n                        const double t"),
+}
+
+
 @pytest.fixture(scope="module")
 def src():
     with open(obuild.SRC) as f:
@@ -54,3 +68,19 @@ def test_mutant_is_caught(name, src, tmp_path):
         except Exception:  # an AssertionError, or an error the mistake provoked
             return
     pytest.fail(f"mutant {name} passed every pin")
+
+
+@pytest.mark.parametrize("name", sorted(KNN_MUTANTS))
+def test_knn_mutant_is_caught(name, src, tmp_path):
+    old, new = KNN_MUTANTS[name]
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(old, new))
+    lib = obuild.build(str(path), str(tmp_path / f"lib_{name}.so"))
+    o = Oracle(lib)
+    for pin in P.KNN_PINS:
+        try:
+            pin(o)
+        except Exception:
+            return
+    pytest.fail(f"mutant {name} passed every KNN pin")

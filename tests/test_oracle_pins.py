@@ -5,7 +5,7 @@ import oracle_pins as P
 from paper_2608_12629_amd.synth import make_workload, raw_bits
 
 
-@pytest.mark.parametrize("pin", P.FAST_PINS, ids=lambda f: f.__name__)
+@pytest.mark.parametrize("pin", P.FAST_PINS + P.KNN_PINS, ids=lambda f: f.__name__)
 def test_pin(oracle, pin):
     pin(oracle)
 
