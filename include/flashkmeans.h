@@ -108,6 +108,27 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
                  int iters, int32_t* idx, float* min_dist, int32_t* counts, double* objective,
                  void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * KNN search (paper Section 6 lists KNN search beside KMeans among its
+ * dispatcher-backed families, with recall 1.0): for every query, the k
+ * database rows at the smallest squared Euclidean distance, nearest first,
+ * ties to the lowest index.  The same fused distance contraction as the
+ * assignment, with a top-k in place of the arg-min; the M x N distance matrix
+ * is never stored.
+ *   Q        [B, M, D] xdtype   queries (read)
+ *   R        [B, N, D] xdtype   database rows (read)
+ *   nbr_idx  [B, M, k] int32    written: row indices, nearest first
+ *   nbr_dist [B, M, k] fp32     written: their squared distances, clamped at 0
+ * xdtype bf16 or fp16 (fp32 is FKM_ERR_UNSUPPORTED); D a multiple of 16 up to
+ * 256; 1 <= k <= min(N, 32) (k > 32 is FKM_ERR_UNSUPPORTED, k > N invalid).
+ * Distances are |q|^2 - 2 <q, r> + |r|^2 with the products accumulated in fp32,
+ * so rows whose distances differ by less than that rounding may trade places.
+ * The workspace holds a staged copy of R: kmeans_knn_workspace_bytes bytes.
+ */
+size_t kmeans_knn_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t D, int k, int xdtype);
+int kmeans_knn(const void* Q, const void* R, int xdtype, int64_t B, int64_t M, int64_t N, int64_t D,
+               int k, int32_t* nbr_idx, float* nbr_dist, void* ws, size_t ws_bytes, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* kmeans_status_string(int status);
 

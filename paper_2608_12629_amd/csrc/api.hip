@@ -159,6 +159,54 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   return FKM_OK;
 }
 
+// ---- KNN search ---------------------------------------------------------------
+static int knn_check_sizes(int64_t B, int64_t M, int64_t N, int64_t D, int64_t k, int dt) {
+  if (B < 1 || M < 1 || N < 1 || D < 1 || k < 1 || k > N) return FKM_ERR_INVALID_ARG;
+  if (dt != DT_F32 && dt != DT_BF16 && dt != DT_F16) return FKM_ERR_INVALID_ARG;
+  if (dt == DT_F32 || D % 16 != 0 || D > 256 || k > KNN_MAX_K) return FKM_ERR_UNSUPPORTED;
+  if (M > INT32_MAX || N > INT32_MAX - ASSIGN_KPAD || B > 65535) return FKM_ERR_UNSUPPORTED;
+  return FKM_OK;
+}
+
+// Workspace: the database rows in the staged layout [B, Np, D] and their
+// scores [B, Np], Np = N rounded up to whole 128-row stages.
+static size_t knn_carve(void* base, int64_t B, int64_t N, int64_t D, void** chat, float** cinit,
+                        int64_t* Np) {
+  *Np = kpad(N);
+  const size_t a = align_up((size_t)(B * *Np * D) * 2);
+  if (base) {
+    *chat = base;
+    *cinit = (float*)((char*)base + a);
+  }
+  return a + align_up((size_t)(B * *Np) * 4);
+}
+
+size_t kmeans_knn_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t D, int k, int xdtype) {
+  if (knn_check_sizes(B, M, N, D, k, xdtype) != FKM_OK) return 0;
+  void* c;
+  float* n;
+  int64_t Np;
+  return knn_carve(nullptr, B, N, D, &c, &n, &Np);
+}
+
+int kmeans_knn(const void* Q, const void* R, int xdtype, int64_t B, int64_t M, int64_t N, int64_t D,
+               int k, int32_t* nbr_idx, float* nbr_dist, void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_ptrs({Q, R, nbr_idx, nbr_dist}))) return rc;
+  if ((rc = knn_check_sizes(B, M, N, D, k, xdtype))) return rc;
+  void* chat = nullptr;
+  float* cinit = nullptr;
+  int64_t Np;
+  if (!ws || !aligned16(ws) || ws_bytes < knn_carve(nullptr, B, N, D, &chat, &cinit, &Np))
+    return FKM_ERR_WORKSPACE;
+  if ((rc = check_device())) return rc;
+  knn_carve(ws, B, N, D, &chat, &cinit, &Np);
+  hipStream_t s = (hipStream_t)stream;
+  if (xdtype == DT_BF16)
+    return hip_status(launch_knn_bf16(Q, R, B, M, N, D, k, chat, cinit, Np, nbr_idx, nbr_dist, s));
+  return hip_status(launch_knn_f16(Q, R, B, M, N, D, k, chat, cinit, Np, nbr_idx, nbr_dist, s));
+}
+
 const char* kmeans_status_string(int status) {
   switch (status) {
     case FKM_OK: return "ok";

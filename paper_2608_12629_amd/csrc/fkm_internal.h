@@ -59,6 +59,8 @@ constexpr int64_t SMALLK_MAX_KD = 16384;
 inline bool smallk_ok(int dt, int64_t D, int64_t K) {
   return K <= (dt == DT_F32 ? 512 : 256) && K * D <= SMALLK_MAX_KD;
 }
+// KNN search: k nearest database rows per query, k <= KNN_MAX_K.
+constexpr int KNN_MAX_K = 32;
 // Limits of this build.
 constexpr int64_t MAX_K = 65536;   // two radix passes of at most 8 bits
 constexpr int64_t MAX_D = 2048;
@@ -127,6 +129,12 @@ hipError_t launch_pipe_bf16(const void* X, const Workspace& w, int64_t B, int64_
                            int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_pipe_f16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
                           int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_knn_bf16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N, int64_t D,
+                          int k, void* chat, float* cinit, int64_t Np, int32_t* nbr_idx,
+                          float* nbr_dist, hipStream_t s);
+hipError_t launch_knn_f16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N, int64_t D,
+                         int k, void* chat, float* cinit, int64_t Np, int32_t* nbr_idx,
+                         float* nbr_dist, hipStream_t s);
 hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,

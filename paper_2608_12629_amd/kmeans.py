@@ -38,7 +38,10 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     lib.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     lib.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
-    for f in (lib.kmeans_assign, lib.kmeans_update, lib.kmeans_lloyd):
+    lib.kmeans_knn_workspace_bytes.argtypes = [i64, i64, i64, i64, i32, i32]
+    lib.kmeans_knn_workspace_bytes.restype = sz
+    lib.kmeans_knn.argtypes = [vp, vp, i32, i64, i64, i64, i64, i32, vp, vp, vp, sz, vp]
+    for f in (lib.kmeans_assign, lib.kmeans_update, lib.kmeans_lloyd, lib.kmeans_knn):
         f.restype = ctypes.c_int
     lib.kmeans_status_string.argtypes = [ctypes.c_int]
     lib.kmeans_status_string.restype = ctypes.c_char_p
@@ -170,3 +173,36 @@ def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
                             _ptr(min_dist), _ptr(counts), _ptr(obj), _ptr(ws.buf), ws.nbytes,
                             _stream()), "kmeans_lloyd")
     return C, idx, min_dist, counts, obj
+
+
+def knn_workspace_bytes(B: int, M: int, N: int, D: int, k: int, dtype: torch.dtype) -> int:
+    return int(lib.kmeans_knn_workspace_bytes(B, M, N, D, k, _DTYPE[dtype]))
+
+
+def kmeans_knn(Q: torch.Tensor, R: torch.Tensor, k: int, nbr_idx: Optional[torch.Tensor] = None,
+               nbr_dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """KNN search: nbr_idx [B,M,k] int32 and nbr_dist [B,M,k] fp32 of the k nearest
+    database rows of every query (see ``kmeans_knn`` in the header)."""
+    if Q.dim() == 2:
+        Q = Q.unsqueeze(0)
+    if R.dim() == 2:
+        R = R.unsqueeze(0)
+    if Q.dim() != 3 or R.dim() != 3 or Q.shape[0] != R.shape[0] or Q.shape[2] != R.shape[2]:
+        raise ValueError(f"shapes Q{tuple(Q.shape)} R{tuple(R.shape)}: want [B,M,D] and [B,N,D]")
+    if Q.dtype != R.dtype:
+        raise TypeError("queries and database must share a dtype")
+    B, M, D = Q.shape
+    N = R.shape[1]
+    _need(Q, "Q")
+    _need(R, "R")
+    dev = Q.device
+    nbr_idx = torch.empty((B, M, k), dtype=torch.int32, device=dev) if nbr_idx is None else nbr_idx
+    nbr_dist = torch.empty((B, M, k), dtype=torch.float32, device=dev) if nbr_dist is None else nbr_dist
+    _need(nbr_idx, "nbr_idx", torch.int32)
+    _need(nbr_dist, "nbr_dist", torch.float32)
+    need = knn_workspace_bytes(B, M, N, D, k, Q.dtype)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check(lib.kmeans_knn(_ptr(Q), _ptr(R), _dt(Q), B, M, N, D, int(k), _ptr(nbr_idx),
+                          _ptr(nbr_dist), _ptr(ws), ws.numel(), _stream()), "kmeans_knn")
+    return nbr_idx, nbr_dist

@@ -31,14 +31,18 @@ def lib():
     L.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     L.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     L.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.kmeans_knn_workspace_bytes.argtypes = [i64, i64, i64, i64, i32, i32]
+    L.kmeans_knn_workspace_bytes.restype = sz
+    L.kmeans_knn.argtypes = [vp, vp, i32, i64, i64, i64, i64, i32, vp, vp, vp, sz, vp]
     L.kmeans_status_string.argtypes = [ctypes.c_int]
     L.kmeans_status_string.restype = ctypes.c_char_p
     return L
 
 
-def test_header_declares_the_four_calls():
-    assert declared_functions() == ["kmeans_assign", "kmeans_lloyd", "kmeans_status_string",
-                                    "kmeans_update", "kmeans_workspace_bytes"]
+def test_header_declares_the_calls():
+    assert declared_functions() == ["kmeans_assign", "kmeans_knn", "kmeans_knn_workspace_bytes",
+                                    "kmeans_lloyd", "kmeans_status_string", "kmeans_update",
+                                    "kmeans_workspace_bytes"]
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -140,3 +144,30 @@ def test_binding_refuses_without_library(tmp_path, monkeypatch):
     with pytest.raises(ImportError):
         km._load()
     importlib.reload(km)  # restore the module state with the real library
+
+
+def _knn(lib, Q=FAKE, R=FAKE, dt=BF16, B=1, M=50, N=100, D=64, k=5, ni=FAKE, nd=FAKE, ws=FAKE,
+         wsb=1 << 40):
+    return lib.kmeans_knn(Q, R, dt, B, M, N, D, k, ni, nd, ws, wsb, None)
+
+
+def test_knn_rejections(lib):
+    assert _knn(lib, Q=None) == EINVAL
+    assert _knn(lib, R=FAKE + 8) == EINVAL
+    assert _knn(lib, ni=None) == EINVAL
+    assert _knn(lib, nd=None) == EINVAL
+    assert _knn(lib, k=0) == EINVAL
+    assert _knn(lib, k=101) == EINVAL         # k > N
+    assert _knn(lib, M=0) == EINVAL
+    assert _knn(lib, dt=3) == EINVAL
+    assert _knn(lib, dt=F32) == EUNSUP        # fp32 search not built
+    assert _knn(lib, D=40) == EUNSUP
+    assert _knn(lib, D=272) == EUNSUP
+    assert _knn(lib, k=33) == EUNSUP
+    assert _knn(lib, ws=None) == EWS
+    assert _knn(lib, wsb=16) == EWS
+    kw = lambda **a: lib.kmeans_knn_workspace_bytes(*[a.get(n, v) for n, v in
+                                                      (("B", 1), ("M", 50), ("N", 100), ("D", 64),
+                                                       ("k", 5), ("dt", BF16))])
+    assert kw() > 0 and kw(k=33) == 0 and kw(dt=F32) == 0
+    assert kw(N=1000) >= kw(N=100)
