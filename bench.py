@@ -74,6 +74,64 @@ def cpu_baseline(w, sample_rows: int):
                       f"full update ({t_update:.2f} s); fp64, OpenMP"}
 
 
+def knn_bench(args):
+    """KNN search (queries/s) on synthetic blobs; one JSON line like the Lloyd bench."""
+    import torch
+    from paper_2608_12629_amd import kmeans as km
+
+    B, M, N, D, k = 1, args.knn_queries, args.knn_rows, 128, args.knn_k
+    g = torch.Generator().manual_seed(7)
+    centres = torch.rand((N // 64, D), generator=g) * 2 - 1
+    R = (centres[torch.randint(0, N // 64, (N,), generator=g)] + 0.1 * torch.randn((N, D), generator=g))
+    Q = (centres[torch.randint(0, N // 64, (M,), generator=g)] + 0.1 * torch.randn((M, D), generator=g))
+    R, Q = R.to(torch.bfloat16), Q.to(torch.bfloat16)
+    dev = torch.device("cuda", 0)
+    Qd, Rd = Q.to(dev), R.to(dev)
+    ni = torch.empty((B, M, k), dtype=torch.int32, device=dev)
+    nd = torch.empty((B, M, k), dtype=torch.float32, device=dev)
+    ws = torch.empty(km.knn_workspace_bytes(B, M, N, D, k, torch.bfloat16), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        km.kmeans_knn(Qd, Rd, k, ni, nd, ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps or 5):
+        km.kmeans_knn(Qd, Rd, k, ni, nd, ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    steps = args.steps or 5
+    ms = e0.elapsed_time(e1) / steps
+    tflops = 2.0 * B * M * N * D / (ms * 1e-3) / 1e12
+    out = {
+        "metric": "KNN search queries/s (k nearest of N rows); distance TFLOP/s as % of MFMA peak",
+        "value": B * M * steps / dt, "unit": "queries/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": dt * 1e3 / steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"knn_m{M}_n{N}_d{D}_k{k}_bf16", "B": B, "M": M, "N": N, "D": D, "k": k},
+        "roofline": {"bound": "mfma", "kernel": "knn", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None},
+    }
+    if not args.no_cpu:
+        import numpy as np
+        from oracle import default
+        from paper_2608_12629_amd.synth import raw_bits
+        o = default()
+        sample = min(M, args.knn_cpu_queries)
+        qs = np.ascontiguousarray(raw_bits(Q[None, :sample]))
+        t0 = time.perf_counter()
+        o.knn(qs, raw_bits(R[None]), "bf16", k)
+        tc = time.perf_counter() - t0
+        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        out["cpu_baseline"] = {"value": sample / tc, "unit": "queries/s", "cores": cores,
+                               "kind": "oracle",
+                               "sample": f"the first {sample} of {M} queries against all {N} rows "
+                                         f"({tc:.2f} s); fp64, OpenMP"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,11 +144,19 @@ def main():
                     help="also run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--workload", type=int, default=3,
                     help="1..5; 3 (N=8M, D=128, K=4096) is the metric workload")
+    ap.add_argument("--knn", action="store_true", help="measure the KNN search instead")
+    ap.add_argument("--knn-queries", type=int, default=262144)
+    ap.add_argument("--knn-rows", type=int, default=1 << 20)
+    ap.add_argument("--knn-k", type=int, default=10)
+    ap.add_argument("--knn-cpu-queries", type=int, default=1536)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(rerun with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+    if args.knn:
+        knn_bench(args)
+        return
 
     import torch
     from paper_2608_12629_amd import kmeans as km

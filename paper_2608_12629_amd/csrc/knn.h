@@ -153,8 +153,10 @@ __device__ __forceinline__ void knn_stage(int st, int nst, char* cur, char* nxt,
   __syncthreads();
 }
 
+// Lists of 8 or 16 fit two waves per SIMD (the update's latency then hides
+// behind the other wave's MFMAs); 32 entries take the whole register file.
 template <int DT, int CPL, int KMAX>
-__global__ __launch_bounds__(ASSIGN_THREADS, KMAX <= 8 ? 2 : 1) void knn_kernel(
+__global__ __launch_bounds__(ASSIGN_THREADS, KMAX <= 16 ? 2 : 1) void knn_kernel(
     const uint4* __restrict__ Q, const uint4* __restrict__ chat, const float* __restrict__ cinit,
     int M, int Np, int k, int32_t* __restrict__ nbr_idx, float* __restrict__ nbr_dist) {
   using L = PipeLayout<CPL>;
@@ -266,6 +268,7 @@ hipError_t launch_knn_dt(const void* Q, const void* R, int64_t B, int64_t M, int
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (k <= 8) return launch_knn_k<DT, 8>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
+  if (k <= 16) return launch_knn_k<DT, 16>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
   return launch_knn_k<DT, KNN_MAX_K>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
 }
 

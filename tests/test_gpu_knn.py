@@ -87,6 +87,7 @@ SHAPES = [
     (1, 257, 129, 256, 8, "bf16"),        # one and a bit stages, widest rows
     (1, 100, 7, 16, 7, "f16"),            # k = N, a database smaller than a tile
     (3, 64, 1000, 96, 16, "bf16"),        # batched
+    (1, 500, 5000, 160, 12, "f16"),       # the 16-entry lists in fp16
 ]
 
 
