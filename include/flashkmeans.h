@@ -31,8 +31,13 @@
  * - Errors: arguments are validated on the host before anything is enqueued;
  *   a rejected call returns a negative status and has no effect.
  *   FKM_ERR_UNSUPPORTED means valid but outside what this build implements:
- *   not gfx950; D not a multiple of 16; D > 2048; bf16/fp16 D above 256 and
- *   not a multiple of 32; fp32 D > 256; K > 65536; N > 2^31-1; B > 65535.
+ *   not gfx950; D > 2048; fp32 D > 256; K > 65536; N > 2^31-1; B > 65535.
+ * - Row widths: the kernels take D a multiple of 16 (and, for bf16/fp16 rows
+ *   wider than 256, of 32).  Any other D is served through copies of the
+ *   points and centroids in zero-padded rows of the next such width, made in
+ *   the workspace at the start of each call (once per kmeans_lloyd call):
+ *   zeros change no distance, sum or norm, so the results are those of the
+ *   unpadded rows, at the cost of that copy.
  *   FKM_ERR_HIP reports a failed HIP call or launch.  No C++ exception
  *   crosses this boundary.
  */
@@ -119,11 +124,13 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
  *   R        [B, N, D] xdtype   database rows (read)
  *   nbr_idx  [B, M, k] int32    written: row indices, nearest first
  *   nbr_dist [B, M, k] fp32     written: their squared distances, clamped at 0
- * xdtype bf16 or fp16 (fp32 is FKM_ERR_UNSUPPORTED); D a multiple of 16 up to
- * 256; 1 <= k <= min(N, 32) (k > 32 is FKM_ERR_UNSUPPORTED, k > N invalid).
+ * xdtype bf16 or fp16 (fp32 is FKM_ERR_UNSUPPORTED); D up to 256 (a D that is
+ * not a multiple of 16 runs on zero-padded copies of the rows, as above);
+ * 1 <= k <= min(N, 32) (k > 32 is FKM_ERR_UNSUPPORTED, k > N invalid).
  * Distances are |q|^2 - 2 <q, r> + |r|^2 with the products accumulated in fp32,
  * so rows whose distances differ by less than that rounding may trade places.
- * The workspace holds a staged copy of R: kmeans_knn_workspace_bytes bytes.
+ * The workspace holds a staged copy of R (and the padded queries):
+ * kmeans_knn_workspace_bytes bytes.
  */
 size_t kmeans_knn_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t D, int k, int xdtype);
 int kmeans_knn(const void* Q, const void* R, int xdtype, int64_t B, int64_t M, int64_t N, int64_t D,

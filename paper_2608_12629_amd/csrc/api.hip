@@ -12,8 +12,12 @@ namespace fkm {
 
 static size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
-Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
+// The workspace for rows of D elements; every kernel runs at w.Dk (equal to D
+// unless D needs zero-padded copies of the points and centroids).
+Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int dt) {
   Workspace w{};
+  const int64_t D = kernel_dim(dt, D_user);
+  w.Dk = D;
   if (assign_tiled(dt, D)) {
     w.n_assign_blocks = (N + 255) / 256;  // the decode kernel's blocks
   } else {
@@ -51,6 +55,9 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt) 
   const bool tiled = assign_tiled(dt, D);
   w.keys = (uint64_t*)take(tiled ? (size_t)(B * N + 1) * 8 + TILED_ZERO_BYTES : 0);
   w.xnorm = (float*)take(tiled ? (size_t)(B * N) * 4 : 0);
+  const bool pad = D != D_user;
+  w.xpad = take(pad ? (size_t)(B * N * D) * dt_bytes(dt) : 0);
+  w.cpad = (float*)take(pad ? (size_t)(B * K * D) * 4 : 0);
   w.total = o;
   return w;
 }
@@ -62,8 +69,27 @@ static int check_sizes(int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
   if (B < 1 || N < 1 || D < 1 || K < 1) return FKM_ERR_INVALID_ARG;
   if (dt != DT_F32 && dt != DT_BF16 && dt != DT_F16) return FKM_ERR_INVALID_ARG;
   if (N > INT32_MAX || K > MAX_K || D > MAX_D || B > 65535) return FKM_ERR_UNSUPPORTED;
-  if (!row_bytes_ok(dt, D) || !assign_ok(dt, D)) return FKM_ERR_UNSUPPORTED;
+  if (kernel_dim(dt, D) == 0) return FKM_ERR_UNSUPPORTED;
   return FKM_OK;
+}
+
+// Points (and centroids, when given) into the workspace's zero-padded rows
+// when the kernels run at a wider row than D; the pointers the kernels read.
+struct KernelArgs {
+  const void* X;
+  float* C;
+};
+static hipError_t pad_inputs(const void* X, const float* C, int dt, const Workspace& w,
+                             int64_t B, int64_t N, int64_t D, int64_t K, KernelArgs* a,
+                             hipStream_t s) {
+  a->X = X;
+  a->C = const_cast<float*>(C);
+  if (w.Dk == D) return hipSuccess;
+  hipError_t e = launch_pad_rows(X, B * N, D, w.Dk, dt_bytes(dt), w.xpad, s);
+  if (e == hipSuccess && C) e = launch_pad_rows(C, B * K, D, w.Dk, 4, w.cpad, s);
+  a->X = w.xpad;
+  a->C = w.cpad;
+  return e;
 }
 
 static int check_ptrs(std::initializer_list<const void*> ps) {
@@ -120,8 +146,10 @@ int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t 
   if ((rc = check_device())) return rc;
   hipStream_t s = (hipStream_t)stream;
   const Workspace w = carve(ws, B, N, D, K, xdtype);
-  if ((rc = hip_status(launch_prep(C, xdtype, B, K, w.Kp, D, w.chat, w.cinit, s)))) return rc;
-  return hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s));
+  KernelArgs a;
+  if ((rc = hip_status(pad_inputs(X, C, xdtype, w, B, N, D, K, &a, s)))) return rc;
+  if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, w.Dk, w.chat, w.cinit, s)))) return rc;
+  return hip_status(launch_assign(a.X, xdtype, w, B, N, w.Dk, K, idx, min_dist, s));
 }
 
 int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_prev, int64_t B,
@@ -132,9 +160,16 @@ int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_
   if ((rc = check_sizes(B, N, D, K, xdtype))) return rc;
   if ((rc = check_ws(ws, ws_bytes, B, N, D, K, xdtype))) return rc;
   if ((rc = check_device())) return rc;
+  hipStream_t s = (hipStream_t)stream;
   const Workspace w = carve(ws, B, N, D, K, xdtype);
-  return hip_status(launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts,
-                                  (hipStream_t)stream));
+  KernelArgs a;
+  if ((rc = hip_status(pad_inputs(X, C_prev, xdtype, w, B, N, D, K, &a, s)))) return rc;
+  if (w.Dk == D)
+    return hip_status(launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts, s));
+  // padded rows: update the padded copy in place, then write its first D columns
+  if ((rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, w.Dk, K, a.C, counts, s))))
+    return rc;
+  return hip_status(launch_unpad_rows(a.C, B * K, w.Dk, D, C_out, s));
 }
 
 int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D, int64_t K,
@@ -149,13 +184,18 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   if ((rc = check_device())) return rc;
   hipStream_t s = (hipStream_t)stream;
   const Workspace w = carve(ws, B, N, D, K, xdtype);
+  // padded rows are copied once; the iterations run on the copies
+  KernelArgs a;
+  if ((rc = hip_status(pad_inputs(X, C, xdtype, w, B, N, D, K, &a, s)))) return rc;
+  const int64_t Dk = w.Dk;
   for (int t = 0; t < iters; ++t) {
-    if ((rc = hip_status(launch_prep(C, xdtype, B, K, w.Kp, D, w.chat, w.cinit, s)))) return rc;
-    if ((rc = hip_status(launch_assign(X, xdtype, w, B, N, D, K, idx, min_dist, s)))) return rc;
+    if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
+    if ((rc = hip_status(launch_assign(a.X, xdtype, w, B, N, Dk, K, idx, min_dist, s)))) return rc;
     if (objective && (rc = hip_status(launch_objective(w, B, iters, t, objective, s)))) return rc;
-    if ((rc = hip_status(launch_update(X, xdtype, idx, C, w, B, N, D, K, C, counts, s))))
+    if ((rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, s))))
       return rc;
   }
+  if (Dk != D) return hip_status(launch_unpad_rows(a.C, B * K, Dk, D, C, s));
   return FKM_OK;
 }
 
@@ -163,30 +203,43 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
 static int knn_check_sizes(int64_t B, int64_t M, int64_t N, int64_t D, int64_t k, int dt) {
   if (B < 1 || M < 1 || N < 1 || D < 1 || k < 1 || k > N) return FKM_ERR_INVALID_ARG;
   if (dt != DT_F32 && dt != DT_BF16 && dt != DT_F16) return FKM_ERR_INVALID_ARG;
-  if (dt == DT_F32 || D % 16 != 0 || D > 256 || k > KNN_MAX_K) return FKM_ERR_UNSUPPORTED;
+  if (dt == DT_F32 || D > 256 || k > KNN_MAX_K) return FKM_ERR_UNSUPPORTED;
   if (M > INT32_MAX || N > INT32_MAX - ASSIGN_KPAD || B > 65535) return FKM_ERR_UNSUPPORTED;
   return FKM_OK;
 }
 
-// Workspace: the database rows in the staged layout [B, Np, D] and their
-// scores [B, Np], Np = N rounded up to whole 128-row stages.
-static size_t knn_carve(void* base, int64_t B, int64_t N, int64_t D, void** chat, float** cinit,
-                        int64_t* Np) {
-  *Np = kpad(N);
-  const size_t a = align_up((size_t)(B * *Np * D) * 2);
-  if (base) {
-    *chat = base;
-    *cinit = (float*)((char*)base + a);
-  }
-  return a + align_up((size_t)(B * *Np) * 4);
+// Workspace: the database rows in the staged layout [B, Np, Dk] and their
+// scores [B, Np], Np = N rounded up to whole 128-row stages, Dk = D rounded up
+// to a multiple of 16; when Dk != D also the queries in zero-padded rows
+// [B, M, Dk].
+struct KnnWs {
+  void* chat;
+  float* cinit;
+  void* qpad;
+  int64_t Np, Dk;
+  size_t total;
+};
+static KnnWs knn_carve(void* base, int64_t B, int64_t M, int64_t N, int64_t D) {
+  KnnWs w{};
+  w.Np = kpad(N);
+  w.Dk = (D + 15) / 16 * 16;
+  char* p = (char*)base;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    char* r = p ? p + o : nullptr;
+    o = align_up(o + bytes);
+    return r;
+  };
+  w.chat = take((size_t)(B * w.Np * w.Dk) * 2);
+  w.cinit = (float*)take((size_t)(B * w.Np) * 4);
+  w.qpad = take(w.Dk != D ? (size_t)(B * M * w.Dk) * 2 : 0);
+  w.total = o;
+  return w;
 }
 
 size_t kmeans_knn_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t D, int k, int xdtype) {
   if (knn_check_sizes(B, M, N, D, k, xdtype) != FKM_OK) return 0;
-  void* c;
-  float* n;
-  int64_t Np;
-  return knn_carve(nullptr, B, N, D, &c, &n, &Np);
+  return knn_carve(nullptr, B, M, N, D).total;
 }
 
 int kmeans_knn(const void* Q, const void* R, int xdtype, int64_t B, int64_t M, int64_t N, int64_t D,
@@ -194,17 +247,21 @@ int kmeans_knn(const void* Q, const void* R, int xdtype, int64_t B, int64_t M, i
   int rc;
   if ((rc = check_ptrs({Q, R, nbr_idx, nbr_dist}))) return rc;
   if ((rc = knn_check_sizes(B, M, N, D, k, xdtype))) return rc;
-  void* chat = nullptr;
-  float* cinit = nullptr;
-  int64_t Np;
-  if (!ws || !aligned16(ws) || ws_bytes < knn_carve(nullptr, B, N, D, &chat, &cinit, &Np))
+  if (!ws || !aligned16(ws) || ws_bytes < knn_carve(nullptr, B, M, N, D).total)
     return FKM_ERR_WORKSPACE;
   if ((rc = check_device())) return rc;
-  knn_carve(ws, B, N, D, &chat, &cinit, &Np);
+  const KnnWs w = knn_carve(ws, B, M, N, D);
   hipStream_t s = (hipStream_t)stream;
+  const void* Qk = Q;
+  if (w.Dk != D) {
+    if ((rc = hip_status(launch_pad_rows(Q, B * M, D, w.Dk, 2, w.qpad, s)))) return rc;
+    Qk = w.qpad;
+  }
   if (xdtype == DT_BF16)
-    return hip_status(launch_knn_bf16(Q, R, B, M, N, D, k, chat, cinit, Np, nbr_idx, nbr_dist, s));
-  return hip_status(launch_knn_f16(Q, R, B, M, N, D, k, chat, cinit, Np, nbr_idx, nbr_dist, s));
+    return hip_status(launch_knn_bf16(Qk, R, B, M, N, D, w.Dk, k, w.chat, w.cinit, w.Np, nbr_idx,
+                                      nbr_dist, s));
+  return hip_status(launch_knn_f16(Qk, R, B, M, N, D, w.Dk, k, w.chat, w.cinit, w.Np, nbr_idx,
+                                   nbr_dist, s));
 }
 
 const char* kmeans_status_string(int status) {

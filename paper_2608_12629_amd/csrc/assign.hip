@@ -293,6 +293,44 @@ hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, i
   return launch_resident_dt<DT_F32>(X, w, B, N, D, K, idx, min_dist, s);
 }
 
+// Row width change for rows whose width the kernels do not take: each block
+// copies PAD_ROWS rows of width Din into rows of width Dout (zeros past Din).
+constexpr int PAD_ROWS = 64;
+template <typename T>
+__global__ __launch_bounds__(256) void pad_rows_kernel(const T* __restrict__ src, int64_t rows,
+                                                       int Din, int Dout, T* __restrict__ dst) {
+  const int64_t r0 = (int64_t)blockIdx.x * PAD_ROWS;
+  const int64_t left = rows - r0;
+  const int nr = left < PAD_ROWS ? (int)left : PAD_ROWS;
+  src += r0 * Din;
+  dst += r0 * Dout;
+  const unsigned total = (unsigned)nr * (unsigned)Dout;
+  for (unsigned j = threadIdx.x; j < total; j += 256) {
+    const unsigned r = j / (unsigned)Dout, d = j - r * (unsigned)Dout;
+    dst[j] = (int)d < Din ? src[(size_t)r * Din + d] : T(0);
+  }
+}
+
+hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk, int elem_bytes,
+                           void* dst, hipStream_t s) {
+  const dim3 grid((unsigned)((rows + PAD_ROWS - 1) / PAD_ROWS));
+  if (elem_bytes == 2)
+    pad_rows_kernel<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)src, rows, (int)D, (int)Dk,
+                                                   (uint16_t*)dst);
+  else
+    pad_rows_kernel<uint32_t><<<grid, 256, 0, s>>>((const uint32_t*)src, rows, (int)D, (int)Dk,
+                                                   (uint32_t*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
+                             hipStream_t s) {
+  const dim3 grid((unsigned)((rows + PAD_ROWS - 1) / PAD_ROWS));
+  pad_rows_kernel<uint32_t><<<grid, 256, 0, s>>>((const uint32_t*)src, rows, (int)Dk, (int)D,
+                                                 (uint32_t*)dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
                             hipStream_t s) {
   objective_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(w.objpart, (int)w.n_assign_blocks,

@@ -42,6 +42,9 @@ namespace fkm {
 // equal upper bits the lowest position wins), and a strict compare on the
 // masked value keeps the earliest tile.  Scores within 16 ulp of each other
 // therefore count as ties and go to the lowest index; nothing else changes.
+// Since |s'| is up to about Q, that window (and the error of min_dist) is
+// relative to the workgroup's largest norm; rows of 16 elements subtract each
+// point's own bound instead (below).
 // Padding rows score -FLT_MAX (an infinity with position bits would be a
 // signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
 typedef __attribute__((address_space(1))) void global_void;
@@ -130,16 +133,19 @@ __device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 
   }
 }
 
-// Packed-key arg-max of one tile into the running (best, code) of each column tile.
-template <int NSUB>
+// Packed-key arg-max of one tile into the running (best, code) of each column
+// tile.  PPQ: the scores are shifted here, by each point's own Qp.
+template <int NSUB, bool PPQ>
 __device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_t tcode,
-                                              float (&best)[NSUB], uint32_t (&code)[NSUB]) {
+                                              float (&best)[NSUB], uint32_t (&code)[NSUB],
+                                              const float (&Qp)[NSUB]) {
 #pragma unroll
   for (int p = 0; p < NSUB; ++p) {
     float k[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j)
-      k[j] = __uint_as_float((__float_as_uint(acc[p][j]) & ~15u) | (uint32_t)j);
+      k[j] = __uint_as_float((__float_as_uint(PPQ ? acc[p][j] - Qp[p] : acc[p][j]) & ~15u) |
+                             (uint32_t)j);
     const float t0 = __builtin_fmaxf(__builtin_fmaxf(k[0], k[1]), k[2]);
     const float t1 = __builtin_fmaxf(__builtin_fmaxf(k[3], k[4]), k[5]);
     const float t2 = __builtin_fmaxf(__builtin_fmaxf(k[6], k[7]), k[8]);
@@ -158,11 +164,12 @@ __device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_
 // One stage in `cur`: start the next stage into `nxt`, run the stage's tiles
 // (tile i on one accumulator set beside the epilogue of tile i-1 on the
 // other), store the next stage's scores, then wait for the loads and sync.
-template <int DT, int CPL, int NSUB, int LOADS>
+template <int DT, int CPL, int NSUB, int LOADS, bool PPQ>
 __device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
                                            const uint4 (&xr)[NSUB][CPL], char* cur, char* nxt,
                                            const PipeOffsets<CPL, LOADS>& o, const u32x4* chat,
-                                           const float* cinit, float Q, int tid,
+                                           const float* cinit, float Q,
+                                           const float (&Qp)[NSUB], int tid,
                                            uint32_t& prev_code, float (&best)[NSUB],
                                            uint32_t (&code)[NSUB]) {
   using L = PipeLayout<CPL>;
@@ -172,14 +179,14 @@ __device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB
   __builtin_amdgcn_sched_barrier(0);
   const uint32_t tb = (uint32_t)(L::TILES * st);
   pipe_mfma_tile<DT, 0, CPL, NSUB, LOADS>(accB, xr, cur, o);
-  pipe_epilogue<NSUB>(accA, prev_code, best, code);
+  pipe_epilogue<NSUB, PPQ>(accA, prev_code, best, code, Qp);
   pipe_mfma_tile<DT, 1, CPL, NSUB, LOADS>(accA, xr, cur, o);
-  pipe_epilogue<NSUB>(accB, tb << 4, best, code);
+  pipe_epilogue<NSUB, PPQ>(accB, tb << 4, best, code, Qp);
   if constexpr (L::TILES == 4) {
     pipe_mfma_tile<DT, 2, CPL, NSUB, LOADS>(accB, xr, cur, o);
-    pipe_epilogue<NSUB>(accA, (tb + 1) << 4, best, code);
+    pipe_epilogue<NSUB, PPQ>(accA, (tb + 1) << 4, best, code, Qp);
     pipe_mfma_tile<DT, 3, CPL, NSUB, LOADS>(accA, xr, cur, o);
-    pipe_epilogue<NSUB>(accB, (tb + 2) << 4, best, code);
+    pipe_epilogue<NSUB, PPQ>(accB, (tb + 2) << 4, best, code, Qp);
   }
   prev_code = (tb + L::TILES - 1) << 4;
   lds_at<float>(nxt, o.n_store, 0) = nn - Q;
@@ -209,6 +216,11 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
   constexpr int PPB = 4 * PPW;             // points per workgroup
   constexpr int LOADS = L::TCS * L::RCP / ASSIGN_THREADS;
   static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * L::RCP, "stage must split evenly");
+  // Rows of 16 elements shift each point's scores by its own bound: their
+  // norms spread too widely for one shift per workgroup (the 16-ulp tie window
+  // would be wide against the smallest points' distances).  Wider rows take
+  // the workgroup's shift, folded into the stored scores at no cost per tile.
+  constexpr bool PPQ = CPL == 1;
 
   __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
   __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
@@ -252,8 +264,12 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
   for (int msk = 1; msk < 64; msk <<= 1) xmax = __builtin_fmaxf(xmax, __shfl_xor(xmax, msk));
   if (lane == 0) lds_q[wave] = xmax;
   __syncthreads();
-  // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding)
-  const float Q = __builtin_fmaf(
+  // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding);
+  // with PPQ each point's own |x|^2 / 2 (the same margin) and Q = 0
+  float Qp[NSUB];
+#pragma unroll
+  for (int p = 0; p < NSUB; ++p) Qp[p] = __builtin_fmaf(0.5f * xn[p], 1.0f + 0x1p-8f, 1e-30f);
+  const float Q = PPQ ? 0.f : __builtin_fmaf(
       0.5f * __builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])),
       1.0f + 0x1p-8f, 1e-30f);
 
@@ -278,15 +294,16 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
   __syncthreads();
   int st = 0;
   for (; st + 2 <= nst; st += 2) {   // two stages per trip: each buffer is a fixed array
-    pipe_stage<DT, CPL, NSUB, LOADS>(st, st + 1, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q,
-                                     tid, prev_code, best, code);
-    pipe_stage<DT, CPL, NSUB, LOADS>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr, buf1,
-                                     buf0, o, chat4, cinit, Q, tid, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st + 1, accA, accB, xr, buf0, buf1, o, chat4, cinit,
+                                          Q, Qp, tid, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr,
+                                          buf1, buf0, o, chat4, cinit, Q, Qp, tid, prev_code, best,
+                                          code);
   }
   if (st < nst)
-    pipe_stage<DT, CPL, NSUB, LOADS>(st, st, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q, tid,
-                                     prev_code, best, code);
-  pipe_epilogue<NSUB>(accA, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q,
+                                          Qp, tid, prev_code, best, code);
+  pipe_epilogue<NSUB, PPQ>(accA, prev_code, best, code, Qp);
 
   double obj = 0.0;
 #pragma unroll
@@ -301,7 +318,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
     i = take ? io : i;
     const int pt = pbase + p * 32 + n;
     if (h == 0 && pt < N) {
-      const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Q, xn[p]), 0.f);
+      const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + (PPQ ? Qp[p] : Q), xn[p]), 0.f);
       idx[pt] = i;
       min_dist[pt] = md;
       obj += (double)md;

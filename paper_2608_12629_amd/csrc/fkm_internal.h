@@ -87,6 +87,16 @@ inline int64_t assign_points_per_block(int dt, int64_t D) {
 inline bool assign_resident_ok(int dt, int64_t D) { return D % 16 == 0 && D >= 16 && D <= 256; }
 inline bool assign_tiled(int dt, int64_t D) { return dt != DT_F32 && D > 256 && D % 32 == 0; }
 inline bool assign_ok(int dt, int64_t D) { return assign_resident_ok(dt, D) || assign_tiled(dt, D); }
+// The row width the kernels run at: D itself when they take it, else D
+// rounded up to a multiple of 16 (32 for 16-bit rows wider than 256), with the
+// points and centroids copied into zero-padded rows first (zeros change no
+// distance, sum or norm).  0 when no kernel takes the rounded width either.
+inline int64_t kernel_dim(int dt, int64_t D) {
+  if (D < 1 || D > MAX_D) return 0;
+  if (row_bytes_ok(dt, D) && assign_ok(dt, D)) return D;
+  const int64_t Dk = D <= 256 ? (D + 15) / 16 * 16 : (D + 31) / 32 * 32;
+  return row_bytes_ok(dt, Dk) && assign_ok(dt, Dk) ? Dk : 0;
+}
 // Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
 // workgroup; its centroids are padded to whole blocks.
 constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 4;
@@ -114,6 +124,9 @@ struct Workspace {
   int32_t* pcount; // [B,n_sk_chunks,K] per-chunk cluster counts (small-K update only)
   uint64_t* keys;  // [B,N] best (score, index) of each point, then TILED_ZERO_BYTES of zeros (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
+  void* xpad;      // [B,N,Dk] the points in zero-padded rows (only when Dk != D)
+  float* cpad;     // [B,K,Dk] the centroids in zero-padded rows (only when Dk != D)
+  int64_t Dk;      // the row width the kernels run at (kernel_dim)
   int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr, n_sk_chunks;
   size_t total;
 };
@@ -129,14 +142,19 @@ hipError_t launch_pipe_bf16(const void* X, const Workspace& w, int64_t B, int64_
                            int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_pipe_f16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
                           int32_t* idx, float* min_dist, hipStream_t s);
-hipError_t launch_knn_bf16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N, int64_t D,
-                          int k, void* chat, float* cinit, int64_t Np, int32_t* nbr_idx,
-                          float* nbr_dist, hipStream_t s);
-hipError_t launch_knn_f16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N, int64_t D,
-                         int k, void* chat, float* cinit, int64_t Np, int32_t* nbr_idx,
-                         float* nbr_dist, hipStream_t s);
+// KNN: R rows of Din elements; Q rows and the staged rows of D >= Din (a multiple of 16)
+hipError_t launch_knn_bf16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N,
+                           int64_t Din, int64_t D, int k, void* chat, float* cinit, int64_t Np,
+                           int32_t* nbr_idx, float* nbr_dist, hipStream_t s);
+hipError_t launch_knn_f16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N,
+                          int64_t Din, int64_t D, int k, void* chat, float* cinit, int64_t Np,
+                          int32_t* nbr_idx, float* nbr_dist, hipStream_t s);
 hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_t B, int64_t N,
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk, int elem_bytes,
+                           void* dst, hipStream_t s);
+hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
+                             hipStream_t s);
 hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
                             hipStream_t s);
 hipError_t update_init();

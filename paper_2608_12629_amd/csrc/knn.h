@@ -30,11 +30,12 @@
 namespace fkm {
 
 // Database rows to the staged layout: row j of each instance to chat (padded to
-// Np rows: zero rows with score -FLT_MAX), and its -|r|^2/2 (one wave per row,
-// lane-strided then a fixed xor butterfly).
+// Np rows: zero rows with score -FLT_MAX; rows of Din elements widened to D
+// with zeros), and its -|r|^2/2 (one wave per row, lane-strided then a fixed
+// xor butterfly).
 template <int DT>
 __global__ __launch_bounds__(256) void knn_prep_kernel(const uint16_t* __restrict__ R, int64_t B,
-                                                       int N, int Np, int D,
+                                                       int N, int Np, int Din, int D,
                                                        uint16_t* __restrict__ chat,
                                                        float* __restrict__ cinit) {
   const int lane = threadIdx.x & 63;
@@ -43,11 +44,11 @@ __global__ __launch_bounds__(256) void knn_prep_kernel(const uint16_t* __restric
   const int64_t b = row / Np;
   const int j = (int)(row % Np);
   const bool pad = j >= N;
-  const uint16_t* r = R + (b * N + (pad ? 0 : j)) * D;
+  const uint16_t* r = R + (b * N + (pad ? 0 : j)) * Din;
   uint16_t* out = chat + row * D;
   float ss = 0.f;
   for (int d = lane; d < D; d += 64) {
-    const uint16_t h = pad ? (uint16_t)0 : r[d];
+    const uint16_t h = (pad || d >= Din) ? (uint16_t)0 : r[d];
     out[d] = h;
     const float v = Elem<DT>::widen(h);
     ss = __builtin_fmaf(v, v, ss);
@@ -256,15 +257,16 @@ hipError_t launch_knn_k(const void* Q, const void* chat, const float* cinit, int
   }
 }
 
-// prep + search for one storage type; k <= KNN_MAX_K, D % 16 == 0, D <= 256.
+// prep + search for one storage type; k <= KNN_MAX_K.  R has rows of Din
+// elements, Q (already padded) and the staged rows have D, D % 16 == 0, D <= 256.
 template <int DT>
-hipError_t launch_knn_dt(const void* Q, const void* R, int64_t B, int64_t M, int64_t N, int64_t D,
-                         int k, void* chat, float* cinit, int64_t Np, int32_t* nbr_idx,
-                         float* nbr_dist, hipStream_t s) {
-  if (D % 16 != 0 || D > 256 || k < 1 || k > KNN_MAX_K || Np % ASSIGN_KPAD != 0)
+hipError_t launch_knn_dt(const void* Q, const void* R, int64_t B, int64_t M, int64_t N,
+                         int64_t Din, int64_t D, int k, void* chat, float* cinit, int64_t Np,
+                         int32_t* nbr_idx, float* nbr_dist, hipStream_t s) {
+  if (D % 16 != 0 || D > 256 || Din > D || k < 1 || k > KNN_MAX_K || Np % ASSIGN_KPAD != 0)
     return hipErrorInvalidValue;
   knn_prep_kernel<DT><<<dim3((unsigned)((B * Np + 3) / 4)), 256, 0, s>>>(
-      (const uint16_t*)R, B, (int)N, (int)Np, (int)D, (uint16_t*)chat, cinit);
+      (const uint16_t*)R, B, (int)N, (int)Np, (int)Din, (int)D, (uint16_t*)chat, cinit);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (k <= 8) return launch_knn_k<DT, 8>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);

@@ -74,7 +74,13 @@ def test_workspace_bytes(lib):
     assert ws(4, 1000, 64, 10) >= ws(1, 1000, 64, 10)
     # rejected shapes report 0
     assert ws(0, 10, 64, 4) == 0 and ws(1, 0, 64, 4) == 0 and ws(1, 10, 64, 0) == 0
-    assert ws(1, 10, 40, 4) == 0            # D not a multiple of 16
+    for D in (1, 3, 40, 100, 250, 272, 300, 2047):
+        assert ws(1, 1000, D, 10) > 0, D    # served on zero-padded rows
+    assert ws(1, 1000, 40, 10) > ws(1, 1000, 48, 10)  # plus the padded copies
+    for D in (3, 17, 255):
+        assert ws(1, 1000, D, 10, F32) > 0, D
+    assert ws(1, 1000, 272, 10, F32) == 0   # fp32 rows past 256
+    assert ws(1, 1000, 2049, 10) == 0
     for D in (16, 48, 96, 160, 208, 256, 288, 384, 640, 992, 2048):
         assert ws(1, 1000, D, 10) > 0, D    # 16-bit shapes in the domain
     for D in (16, 48, 80, 112, 128, 144, 256):
@@ -111,9 +117,8 @@ def test_rejections_before_any_device_call(lib, call):
     assert call(lib, N=-5) == EINVAL
     assert call(lib, K=0) == EINVAL
     assert call(lib, D=0) == EINVAL
-    assert call(lib, D=40) == EUNSUP          # not a multiple of 16
     assert call(lib, D=4096) == EUNSUP
-    assert call(lib, D=272) == EUNSUP         # 16-bit rows past 256 must be multiples of 32
+    assert call(lib, D=2049) == EUNSUP
     assert call(lib, dt=F32, D=272) == EUNSUP  # fp32 rows up to 256
     assert call(lib, K=70000) == EUNSUP
     assert call(lib, N=1 << 31) == EUNSUP
@@ -161,7 +166,6 @@ def test_knn_rejections(lib):
     assert _knn(lib, M=0) == EINVAL
     assert _knn(lib, dt=3) == EINVAL
     assert _knn(lib, dt=F32) == EUNSUP        # fp32 search not built
-    assert _knn(lib, D=40) == EUNSUP
     assert _knn(lib, D=272) == EUNSUP
     assert _knn(lib, k=33) == EUNSUP
     assert _knn(lib, ws=None) == EWS

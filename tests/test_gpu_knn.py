@@ -88,6 +88,8 @@ SHAPES = [
     (1, 100, 7, 16, 7, "f16"),            # k = N, a database smaller than a tile
     (3, 64, 1000, 96, 16, "bf16"),        # batched
     (1, 500, 5000, 160, 12, "f16"),       # the 16-entry lists in fp16
+    (1, 300, 2000, 40, 5, "bf16"),        # D = 40: zero-padded copies to 48
+    (2, 200, 1500, 100, 20, "f16"),       # D = 100 -> 112, batched
 ]
 
 

@@ -34,8 +34,15 @@ def km():
     return kmeans
 
 
-def teacher_forced(km, o, X, C0, dtype, iters, rows=None):
-    """Run `iters` assign/update steps on the GPU and check each against the oracle."""
+def teacher_forced(km, o, X, C0, dtype, iters, rows=None, rounded=False):
+    """Run `iters` assign/update steps on the GPU and check each against the oracle.
+
+    rounded: check the assignment against the centroids rounded to the points'
+    type (torch's round-to-nearest-even cast), the ones the kernel measures
+    distances to.  Over D >= 16 dimensions the rounding errors average out far
+    below the tolerance; over a handful they need not (the bound is
+    2 |x - c| u |c| with u = 2^-8 for bf16), so narrow rows are checked this way.
+    """
     Xd = X.cuda()
     C = C0.cuda().clone()
     Xr = raw(X)
@@ -47,13 +54,14 @@ def teacher_forced(km, o, X, C0, dtype, iters, rows=None):
         C1, n = km.kmeans_update(Xd, idx, C, ws=ws)
         torch.cuda.synchronize()
         C64 = C.cpu().double().numpy()
+        Ca64 = C.cpu().to(X.dtype).double().numpy() if rounded else C64
         ig, mg = idx.cpu().numpy(), md.cpu().numpy()
         if rows is not None:
             ig_s, mg_s = ig[:, rows], mg[:, rows]
         else:
             ig_s, mg_s = ig, mg
-        rep = check_assign(o, Xs, dtype, C64, ig_s, mg_s) if rows is None else \
-            check_assign_rows(o, Xs, dtype, C64, ig_s, mg_s)
+        rep = check_assign(o, Xs, dtype, Ca64, ig_s, mg_s) if rows is None else \
+            check_assign_rows(o, Xs, dtype, Ca64, ig_s, mg_s)
         err = check_update(o, Xr, dtype, ig, C64, C1.cpu().numpy(), n.cpu().numpy())
         say(f"  t={t} mismatches={rep.mismatches} (exempt pts {rep.exempt_points}) "
             f"md_err={rep.worst_md_err:.2e} J={rep.J_gpu:.6e}/{rep.J_oracle:.6e} C_err={err:.2e}")
@@ -144,6 +152,13 @@ SHAPES = [
     (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
     (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
+    # widths the kernels do not take run on zero-padded copies of the rows
+    (1, 1000, 1, 5, "bf16"),          # D = 1 -> 16
+    (1, 3000, 3, 8, "f32"),           # D = 3 -> 16
+    (1, 3000, 40, 30, "bf16"),        # D = 40 -> 48
+    (2, 1500, 100, 70, "f16"),        # D = 100 -> 112, batched
+    (1, 2000, 17, 300, "f32"),        # fp32 D = 17 -> 32, sorted update
+    (1, 900, 300, 100, "bf16"),       # D = 300 -> 320, tiled kernel
 ]
 
 
@@ -152,7 +167,7 @@ def test_edge_shapes(km, oracle, shape):
     B, N, D, K, dt = shape
     X, C0 = _blobs(B, N, D, K, DT[dt], seed=N * 7 + K)
     say(f"[edge] B={B} N={N} D={D} K={K} {dt}")
-    teacher_forced(km, oracle, X, C0, dt, 2)
+    teacher_forced(km, oracle, X, C0, dt, 2, rounded=D < 16 and dt != "f32")
 
 
 def test_duplicates_and_empty_clusters(km, oracle):
@@ -225,6 +240,31 @@ def test_lloyd_equals_steps_and_is_deterministic(km, oracle, cfg, kw):
     # the objective never increases (up to the contract's relative tolerance)
     o = obj_a.cpu().numpy()
     assert np.all(np.diff(o, axis=-1) <= tol_for(w.dtype) * o[:, :-1])
+
+
+@pytest.mark.parametrize("D,Dk,dt", [(40, 48, torch.bfloat16), (3, 16, torch.float32),
+                                      (300, 320, torch.float16)])
+def test_padded_rows_equal_explicit_padding(km, D, Dk, dt):
+    """A width the kernels do not take gives, bit for bit, the results of the
+    same rows padded with zeros by the caller (idx, min_dist, counts, the
+    objective, and C_T's first D columns; its padding columns stay zero)."""
+    X, C0 = _blobs(2, 3000, D, 37, dt, seed=D)
+    Xp = torch.nn.functional.pad(X, (0, Dk - D))
+    Cp = torch.nn.functional.pad(C0, (0, Dk - D))
+    say(f"[padded] D={D} -> {Dk} {dt}")
+    a = km.kmeans_lloyd(X.cuda(), C0.cuda(), 3)
+    b = km.kmeans_lloyd(Xp.cuda(), Cp.cuda(), 3)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0][..., :D]) and not b[0][..., D:].any()
+    for u, v in zip(a[1:], b[1:]):
+        assert torch.equal(u, v)
+    idx, md = km.kmeans_assign(X.cuda(), C0.cuda())
+    idx_p, md_p = km.kmeans_assign(Xp.cuda(), Cp.cuda())
+    C1, n1 = km.kmeans_update(X.cuda(), idx, C0.cuda())
+    C1p, n1p = km.kmeans_update(Xp.cuda(), idx, Cp.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx_p) and torch.equal(md, md_p)
+    assert torch.equal(C1, C1p[..., :D]) and torch.equal(n1, n1p)
 
 
 def test_mass_conservation_full_cfg3(km):
