@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libflashkmeans.so")
 SOURCES = ["api.hip", "assign.hip", "assign_pipe_bf16.hip", "assign_pipe_f16.hip",
-           "assign_tiled.hip", "update.hip", "knn_bf16.hip", "knn_f16.hip"]
+           "assign_smallk_bf16.hip", "assign_smallk_f16.hip", "assign_tiled.hip", "update.hip",
+           "knn_bf16.hip", "knn_f16.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -48,6 +48,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   w.perm = (int32_t*)take((size_t)(B * N) * 4);
   w.carry = (float*)take((size_t)(red_slices_bound(B, N) * 2 * D) * 4);
   w.sums = (float*)take((size_t)(B * K * D) * 4);
+  // per-chunk partials of the small-K update (sums_ok shapes are a subset)
   const bool sk = smallk_ok(dt, D, K);
   w.n_sk_chunks = (N + SMALLK_CH - 1) / SMALLK_CH;
   w.partial = (float*)take(sk ? (size_t)(B * w.n_sk_chunks * K * D) * 4 : 0);
@@ -188,12 +189,25 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   KernelArgs a;
   if ((rc = hip_status(pad_inputs(X, C, xdtype, w, B, N, D, K, &a, s)))) return rc;
   const int64_t Dk = w.Dk;
+  // Small K: one kernel assigns and sums (X read once per iteration), with
+  // the arithmetic of the kernels kmeans_assign and kmeans_update run for
+  // these shapes; their workgroups take SMALLK_CH points each.
+  const bool fused = fused_ok(xdtype, Dk, K);
+  const int64_t nparts = sums_ok(xdtype, Dk, K) ? w.n_sk_chunks : w.n_assign_blocks;
   for (int t = 0; t < iters; ++t) {
     if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
-    if ((rc = hip_status(launch_assign(a.X, xdtype, w, B, N, Dk, K, idx, min_dist, s)))) return rc;
-    if (objective && (rc = hip_status(launch_objective(w, B, iters, t, objective, s)))) return rc;
-    if ((rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, s))))
+    if (fused)
+      rc = hip_status(launch_sums(a.X, xdtype, w, B, N, Dk, K, SUMS_FUSED, idx, min_dist, s));
+    else
+      rc = hip_status(launch_assign(a.X, xdtype, w, B, N, Dk, K, idx, min_dist, s));
+    if (rc) return rc;
+    if (objective && (rc = hip_status(launch_objective(w, nparts, B, iters, t, objective, s))))
       return rc;
+    if (fused)
+      rc = hip_status(launch_combine(w, w.n_sk_chunks, a.C, B, K, Dk, a.C, counts, s));
+    else
+      rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, s));
+    if (rc) return rc;
   }
   if (Dk != D) return hip_status(launch_unpad_rows(a.C, B * K, Dk, D, C, s));
   return FKM_OK;

@@ -288,6 +288,8 @@ hipError_t launch_assign(const void* X, int dt, const Workspace& w, int64_t B, i
                          int64_t D, int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
   if (assign_tiled(dt, D)) return launch_assign_tiled(X, dt, w, B, N, D, idx, min_dist, s);
   if (!assign_resident_ok(dt, D)) return hipErrorInvalidValue;
+  // small K: the kernel of the fused step, without the sums (the same bits)
+  if (sums_ok(dt, D, K)) return launch_sums(X, dt, w, B, N, D, K, SUMS_ASSIGN, idx, min_dist, s);
   if (dt == DT_BF16) return launch_pipe_bf16(X, w, B, N, D, idx, min_dist, s);
   if (dt == DT_F16) return launch_pipe_f16(X, w, B, N, D, idx, min_dist, s);
   return launch_resident_dt<DT_F32>(X, w, B, N, D, K, idx, min_dist, s);
@@ -331,10 +333,17 @@ hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
-                            hipStream_t s) {
-  objective_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(w.objpart, (int)w.n_assign_blocks,
-                                                           iters, t, objective);
+hipError_t launch_sums(const void* X, int dt, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                       int64_t K, int mode, int32_t* idx, float* min_dist, hipStream_t s) {
+  if (dt == DT_BF16) return launch_sums_bf16(X, w, B, N, D, K, mode, idx, min_dist, s);
+  if (dt == DT_F16) return launch_sums_f16(X, w, B, N, D, K, mode, idx, min_dist, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_objective(const Workspace& w, int64_t nparts, int64_t B, int iters, int t,
+                            double* objective, hipStream_t s) {
+  objective_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(w.objpart, (int)nparts, iters, t,
+                                                           objective);
   return hipGetLastError();
 }
 

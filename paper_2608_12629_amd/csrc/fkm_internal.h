@@ -59,6 +59,19 @@ constexpr int64_t SMALLK_MAX_KD = 16384;
 inline bool smallk_ok(int dt, int64_t D, int64_t K) {
   return K <= (dt == DT_F32 ? 512 : 256) && K * D <= SMALLK_MAX_KD;
 }
+// Small-K kernels with one-hot MFMA sums (the assignment, the update's sums
+// and the fused Lloyd step for these shapes): 16-bit rows of 32 to 128
+// elements and at most 8 per-wave 32x32 sum tiles (128 registers): the
+// ceil(K/32) cluster tiles rounded up to 2, 4 or 8, times ceil(D/32).  The
+// fused step holds the sums beside the assignment's registers: at most 4.
+inline int64_t sums_tiles(int64_t D, int64_t K) {
+  const int64_t kt = (K + 31) / 32;
+  return (kt <= 2 ? 2 : (kt <= 4 ? 4 : 8)) * ((D + 31) / 32);
+}
+inline bool sums_ok(int dt, int64_t D, int64_t K) {
+  return dt != DT_F32 && D % 16 == 0 && D >= 32 && D <= 128 && K <= 256 && sums_tiles(D, K) <= 8;
+}
+inline bool fused_ok(int dt, int64_t D, int64_t K) { return sums_ok(dt, D, K) && sums_tiles(D, K) <= 4; }
 // KNN search: k nearest database rows per query, k <= KNN_MAX_K.
 constexpr int KNN_MAX_K = 32;
 // Limits of this build.
@@ -120,8 +133,8 @@ struct Workspace {
   int32_t* perm;   // [B,N] point ids sorted by cluster
   float* carry;    // [B,n_red_chunks,2,D] partial sums of clusters cut by slice ends
   float* sums;     // [B,K,D] sums of clusters that fit in one chunk
-  float* partial;  // [B,n_sk_chunks,K,D] per-chunk cluster sums (small-K update only)
-  int32_t* pcount; // [B,n_sk_chunks,K] per-chunk cluster counts (small-K update only)
+  float* partial;  // [B,nch,K,D] per-chunk cluster sums (small-K update; nch = n_sk_chunks, or n_assign_blocks when sums_ok)
+  int32_t* pcount; // [B,nch,K] per-chunk cluster counts
   uint64_t* keys;  // [B,N] best (score, index) of each point, then TILED_ZERO_BYTES of zeros (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
   void* xpad;      // [B,N,Dk] the points in zero-padded rows (only when Dk != D)
@@ -142,6 +155,19 @@ hipError_t launch_pipe_bf16(const void* X, const Workspace& w, int64_t B, int64_
                            int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_pipe_f16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
                           int32_t* idx, float* min_dist, hipStream_t s);
+// sums_ok shapes, by mode: SUMS_ASSIGN the assignment (idx, min_dist and
+// objective partials, one per SMALLK_CH points), SUMS_FUSED that plus the
+// per-chunk partial sums and counts, SUMS_ONLY the partials of the given idx.
+enum SumsMode { SUMS_ASSIGN = 0, SUMS_FUSED = 1, SUMS_ONLY = 2 };
+hipError_t launch_sums_bf16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                           int64_t K, int mode, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_sums_f16(const void* X, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                          int64_t K, int mode, int32_t* idx, float* min_dist, hipStream_t s);
+hipError_t launch_sums(const void* X, int dt, const Workspace& w, int64_t B, int64_t N, int64_t D,
+                       int64_t K, int mode, int32_t* idx, float* min_dist, hipStream_t s);
+// Means from the per-chunk partials and counts (nch chunks per instance).
+hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
+                          int64_t K, int64_t D, float* C_out, int32_t* counts, hipStream_t s);
 // KNN: R rows of Din elements; Q rows and the staged rows of D >= Din (a multiple of 16)
 hipError_t launch_knn_bf16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N,
                            int64_t Din, int64_t D, int k, void* chat, float* cinit, int64_t Np,
@@ -155,8 +181,9 @@ hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk,
                            void* dst, hipStream_t s);
 hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
                              hipStream_t s);
-hipError_t launch_objective(const Workspace& w, int64_t B, int iters, int t, double* objective,
-                            hipStream_t s);
+// objective[b, t] = sum of the nparts per-workgroup partials of instance b
+hipError_t launch_objective(const Workspace& w, int64_t nparts, int64_t B, int iters, int t,
+                            double* objective, hipStream_t s);
 hipError_t update_init();
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,

@@ -712,9 +712,22 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
   d2 = bits - (passes == 1 ? 0 : d1);
 }
 
+hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
+                          int64_t K, int64_t D, float* C_out, int32_t* counts, hipStream_t s) {
+  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
+      w.partial, w.pcount, C_prev, (int)K, (int)D, (int)nch, C_out, counts);
+  return hipGetLastError();
+}
+
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
                          float* C_out, int32_t* counts, hipStream_t s) {
+  if (sums_ok(dt, D, K)) {
+    const hipError_t e = launch_sums(X, dt, w, B, N, D, K, SUMS_ONLY, const_cast<int32_t*>(idx),
+                                     nullptr, s);
+    if (e != hipSuccess) return e;
+    return launch_combine(w, w.n_sk_chunks, C_prev, B, K, D, C_out, counts, s);
+  }
   if (smallk_ok(dt, D, K))
     return launch_update_smallk(X, dt, idx, C_prev, w, B, N, D, K, C_out, counts, s);
   hipError_t e;

@@ -136,6 +136,8 @@ SHAPES = [
     (2, 6000, 128, 128, "bf16"),      # per-chunk update at K * D = 16384, ragged chunk
     (1, 10000, 32, 512, "f32"),       # per-chunk update, fp32, 9-bit cluster ids
     (1, 3000, 16, 10, "bf16"),        # D = 16: one chunk per lane
+    (1, 4000, 32, 250, "bf16"),       # one-hot sums with 8 cluster tiles
+    (1, 3000, 80, 60, "f16"),         # one-hot sums, odd chunk count (a padded dimension tile)
     (1, 3000, 48, 37, "f16"),         # D = 48: padded LDS rows, masked row lanes
     (2, 1500, 96, 50, "bf16"),        # D = 96
     (1, 2000, 160, 70, "bf16"),       # D = 160: one column tile per wave, padded rows
@@ -265,6 +267,31 @@ def test_padded_rows_equal_explicit_padding(km, D, Dk, dt):
     torch.cuda.synchronize()
     assert torch.equal(idx, idx_p) and torch.equal(md, md_p)
     assert torch.equal(C1, C1p[..., :D]) and torch.equal(n1, n1p)
+
+
+@pytest.mark.parametrize("shape", [(1, 5000, 32, 250, "bf16"), (2, 3000, 128, 64, "f16"),
+                                   (1, 3000, 80, 60, "bf16"), (3, 2000, 48, 33, "f16"),
+                                   (2, 4500, 32, 100, "bf16"), (1, 2100, 64, 64, "f16")],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_fused_lloyd_equals_steps(km, shape):
+    """Small-K shapes (one-hot sums; the last three assign and sum in one
+    kernel): bit-identical to kmeans_assign followed by kmeans_update, and
+    repeatable.  N = 2,100 leaves a 52-point last chunk."""
+    B, N, D, K, dt = shape
+    X, C0 = _blobs(B, N, D, K, DT[dt], seed=N + K)
+    Xd = X.cuda()
+    say(f"[fused] B={B} N={N} D={D} K={K} {dt}")
+    a = km.kmeans_lloyd(Xd, C0.cuda(), 3)
+    b = km.kmeans_lloyd(Xd, C0.cuda(), 3)
+    C = C0.cuda()
+    for t in range(3):
+        idx, md = km.kmeans_assign(Xd, C)
+        C, n = km.kmeans_update(Xd, idx, C)
+    torch.cuda.synchronize()
+    for u, v in zip(a, b):
+        assert torch.equal(u, v), "two identical runs differ"
+    assert torch.equal(a[0], C) and torch.equal(a[1], idx) and torch.equal(a[2], md)
+    assert torch.equal(a[3], n)
 
 
 def test_mass_conservation_full_cfg3(km):
