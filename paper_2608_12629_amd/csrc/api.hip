@@ -166,9 +166,11 @@ int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_
   KernelArgs a;
   if ((rc = hip_status(pad_inputs(X, C_prev, xdtype, w, B, N, D, K, &a, s)))) return rc;
   if (w.Dk == D)
-    return hip_status(launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts, s));
+    return hip_status(
+        launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts, NextStep{}, s));
   // padded rows: update the padded copy in place, then write its first D columns
-  if ((rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, w.Dk, K, a.C, counts, s))))
+  if ((rc = hip_status(
+           launch_update(a.X, xdtype, idx, a.C, w, B, N, w.Dk, K, a.C, counts, NextStep{}, s))))
     return rc;
   return hip_status(launch_unpad_rows(a.C, B * K, w.Dk, D, C_out, s));
 }
@@ -193,20 +195,30 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   // the arithmetic of the kernels kmeans_assign and kmeans_update run for
   // these shapes; their workgroups take SMALLK_CH points each.
   const bool fused = fused_ok(xdtype, Dk, K);
-  const int64_t nparts = sums_ok(xdtype, Dk, K) ? w.n_sk_chunks : w.n_assign_blocks;
+  // The update's last kernel also writes the next iteration's rounded
+  // centroids and scores (prep runs once) and this iteration's objective.
+  NextStep nx;
+  nx.dt = xdtype;
+  nx.chat = w.chat;
+  nx.cinit = w.cinit;
+  nx.Kp = w.Kp;
+  nx.objpart = w.objpart;
+  nx.nparts = sums_ok(xdtype, Dk, K) ? w.n_sk_chunks : w.n_assign_blocks;
+  nx.iters = iters;
+  nx.objective = objective;
+  if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
   for (int t = 0; t < iters; ++t) {
-    if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
+    nx.t = t;
+    if (t + 1 == iters) nx.chat = nullptr;  // no next iteration
     if (fused)
       rc = hip_status(launch_sums(a.X, xdtype, w, B, N, Dk, K, SUMS_FUSED, idx, min_dist, s));
     else
       rc = hip_status(launch_assign(a.X, xdtype, w, B, N, Dk, K, idx, min_dist, s));
     if (rc) return rc;
-    if (objective && (rc = hip_status(launch_objective(w, nparts, B, iters, t, objective, s))))
-      return rc;
     if (fused)
-      rc = hip_status(launch_combine(w, w.n_sk_chunks, a.C, B, K, Dk, a.C, counts, s));
+      rc = hip_status(launch_combine(w, w.n_sk_chunks, a.C, B, K, Dk, a.C, counts, nx, s));
     else
-      rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, s));
+      rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, nx, s));
     if (rc) return rc;
   }
   if (Dk != D) return hip_status(launch_unpad_rows(a.C, B * K, Dk, D, C, s));

@@ -1,9 +1,9 @@
 // assign.hip -- the assignment step of the Lloyd iteration (paper Section 5:
 // squared Euclidean distance of each point to all K centroids, then the
 // arg-min), fused so that the N x K distance matrix is never stored.  This
-// file holds the centroid preparation, the fp32 kernel, the objective pass
-// and the dispatch; the bf16/fp16 kernels are in assign_pipe.h (D <= 256) and
-// assign_tiled.hip (wider rows).
+// file holds the centroid preparation, the fp32 kernel, the row-width copies
+// and the dispatch; the bf16/fp16 kernels are in assign_pipe.h (D <= 256),
+// assign_smallk.h (small K) and assign_tiled.hip (wider rows).
 //
 // For point x and centroid c the kernels maximise
 //     s(x, c) = <x, c^> - |c^|^2 / 2
@@ -38,27 +38,8 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ C, 
   const int64_t b = row / Kp;
   const int k = (int)(row % Kp);
   const bool pad = k >= K;
-  const float* c = C + (b * K + (pad ? 0 : k)) * D;
-  float ss = 0.f;
-  if constexpr (DT == DT_F32) {
-    float* out = (float*)chat + row * D;
-    for (int d = lane; d < D; d += 64) {
-      const float v = pad ? 0.f : c[d];
-      out[d] = v;
-      ss = __builtin_fmaf(v, v, ss);
-    }
-  } else {
-    uint16_t* out = (uint16_t*)chat + row * D;
-    for (int d = lane; d < D; d += 64) {
-      const uint16_t h = pad ? (uint16_t)0 : Elem<DT>::narrow(c[d]);
-      out[d] = h;
-      const float v = Elem<DT>::widen(h);
-      ss = __builtin_fmaf(v, v, ss);
-    }
-  }
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
-  if (lane == 0) cinit[row] = pad ? -0x1.fffffep127f : -0.5f * ss;
+  prep_row<DT>(C + (b * K + (pad ? 0 : k)) * D, pad, D, lane,
+               (char*)chat + row * D * (DT == DT_F32 ? 4 : 2), cinit + row);
 }
 
 // ---------------------------------------------------------------------------
@@ -207,33 +188,6 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
 }
 
 
-// Sum of one instance's workgroup partials in a fixed order, in fp64: thread t
-// sums partials t, t + 1024, ... (eight loads in flight), then a tree in LDS.
-__global__ __launch_bounds__(1024) void objective_kernel(const double* __restrict__ part, int nblk,
-                                                         int iters, int t, double* __restrict__ out) {
-  __shared__ double s[1024];
-  const int b = blockIdx.x;
-  const double* pb = part + (size_t)b * nblk;
-  double a = 0.0;
-  for (int i0 = 0; i0 < nblk; i0 += 8 * 1024) {
-    double v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * 1024 + (int)threadIdx.x;
-      v[u] = i < nblk ? pb[i] : 0.0;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) a += v[u];
-  }
-  s[threadIdx.x] = a;
-  __syncthreads();
-  for (int w = 512; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) out[(size_t)b * iters + t] = s[0];
-}
-
 // ---------------------------------------------------------------------------
 hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp, int64_t D,
                        void* chat, float* cinit, hipStream_t s) {
@@ -340,11 +294,5 @@ hipError_t launch_sums(const void* X, int dt, const Workspace& w, int64_t B, int
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_objective(const Workspace& w, int64_t nparts, int64_t B, int iters, int t,
-                            double* objective, hipStream_t s) {
-  objective_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(w.objpart, (int)nparts, iters, t,
-                                                           objective);
-  return hipGetLastError();
-}
 
 }  // namespace fkm

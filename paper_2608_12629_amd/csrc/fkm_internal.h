@@ -10,7 +10,7 @@ namespace fkm {
 
 enum Dt { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
 
-inline int dt_bytes(int dt) { return dt == DT_F32 ? 4 : 2; }
+__host__ __device__ inline int dt_bytes(int dt) { return dt == DT_F32 ? 4 : 2; }
 constexpr int pow2_at_least(int v) { return v <= 1 ? 1 : 2 * pow2_at_least((v + 1) / 2); }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -146,6 +146,20 @@ struct Workspace {
 
 Workspace carve(void* base, int64_t B, int64_t N, int64_t D, int64_t K, int dt);
 
+// What the update's last kernel also produces inside kmeans_lloyd: the next
+// iteration's assignment inputs (the rounded centroids and their scores, as
+// prep would write them) and the objective of this iteration's assignment.
+struct NextStep {
+  int dt = 0;
+  void* chat = nullptr;          // [B,Kp,D]; nullptr: not written
+  float* cinit = nullptr;        // [B,Kp]
+  int64_t Kp = 0;
+  const double* objpart = nullptr;
+  int64_t nparts = 0;            // objective partials per instance
+  int iters = 0, t = 0;
+  double* objective = nullptr;   // [B,iters]; nullptr: not computed
+};
+
 // ---- launchers (return hipSuccess or the launch error) ----------------------
 hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp, int64_t D,
                        void* chat, float* cinit, hipStream_t s);
@@ -167,7 +181,8 @@ hipError_t launch_sums(const void* X, int dt, const Workspace& w, int64_t B, int
                        int64_t K, int mode, int32_t* idx, float* min_dist, hipStream_t s);
 // Means from the per-chunk partials and counts (nch chunks per instance).
 hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
-                          int64_t K, int64_t D, float* C_out, int32_t* counts, hipStream_t s);
+                          int64_t K, int64_t D, float* C_out, int32_t* counts,
+                          const NextStep& nx, hipStream_t s);
 // KNN: R rows of Din elements; Q rows and the staged rows of D >= Din (a multiple of 16)
 hipError_t launch_knn_bf16(const void* Q, const void* R, int64_t B, int64_t M, int64_t N,
                            int64_t Din, int64_t D, int k, void* chat, float* cinit, int64_t Np,
@@ -181,12 +196,9 @@ hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk,
                            void* dst, hipStream_t s);
 hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
                              hipStream_t s);
-// objective[b, t] = sum of the nparts per-workgroup partials of instance b
-hipError_t launch_objective(const Workspace& w, int64_t nparts, int64_t B, int iters, int t,
-                            double* objective, hipStream_t s);
 hipError_t update_init();
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
-                         float* C_out, int32_t* counts, hipStream_t s);
+                         float* C_out, int32_t* counts, const NextStep& nx, hipStream_t s);
 
 }  // namespace fkm

@@ -11,7 +11,7 @@
 //                 fixed order; a run cut by a chunk end leaves a partial
 //   4. finalize   per cluster, the sum (or its partials, in chunk order) over
 //                 the count; an empty cluster keeps its previous centroid.
-#include "fkm_internal.h"
+#include "fkm_device.h"
 
 namespace fkm {
 
@@ -370,60 +370,96 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
   }
 }
 
+// The tail of the update kernels inside kmeans_lloyd (NextStep): the new
+// centroid row k, staged in LDS by the workgroup, becomes the next
+// iteration's rounded row and score (wave 0, prep_row: the bits prep would
+// write), and the workgroup of cluster 0 sums the instance's objective
+// partials in fp64 in a fixed order.
+__device__ inline void next_step_tail(const NextStep& nx, const float* row, int64_t b, int k, int D,
+                                      int tid, double* red) {
+  if (nx.chat && tid < 64) {
+    const int64_t r = b * nx.Kp + k;
+    void* out = (char*)nx.chat + r * D * dt_bytes(nx.dt);
+    if (nx.dt == DT_BF16) prep_row<DT_BF16>(row, false, D, tid, out, nx.cinit + r);
+    else if (nx.dt == DT_F16) prep_row<DT_F16>(row, false, D, tid, out, nx.cinit + r);
+    else prep_row<DT_F32>(row, false, D, tid, out, nx.cinit + r);
+  }
+  if (nx.objective && k == 0) {
+    const double* pb = nx.objpart + b * nx.nparts;
+    double a = 0.0;
+    for (int64_t i = tid; i < nx.nparts; i += 256) a += pb[i];
+    red[tid] = a;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (tid < w) red[tid] += red[tid + w];
+      __syncthreads();
+    }
+    if (tid == 0) nx.objective[b * nx.iters + nx.t] = red[0];
+  }
+}
+
 // One workgroup per cluster: each thread owns 4 consecutive dimensions; the
 // (256 / (D/4)) row slots split a long list of partials and are combined in
 // a fixed order through LDS.
 __global__ __launch_bounds__(256) void finalize_kernel(
     const float* __restrict__ sums, const float* __restrict__ carry,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ off,
-    const float* C_prev, int K, int D, int nred, int cr, float* C_out) {
-  extern __shared__ float4 part[];
+    const float* C_prev, int K, int D, int nred, int cr, float* C_out, NextStep nx) {
+  __shared__ float4 part[256];
+  __shared__ __attribute__((aligned(16))) float row[MAX_D];
+  __shared__ double red[256];
   const int k = blockIdx.x, b = blockIdx.y;
   const int t = threadIdx.x;
   const int D4 = D / 4;
   const int slots = D4 >= 256 ? 1 : 256 / D4;
   const size_t rowoff = ((size_t)b * K + k) * D;
+  float4* row4 = reinterpret_cast<float4*>(row);
   const int n = counts[(size_t)b * K + k];
-  if (n == 0) {
-    for (int d = t; d < D4; d += 256)
-      reinterpret_cast<float4*>(C_out + rowoff)[d] = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
-    return;
-  }
   const int j0 = off[(size_t)b * (K + 1) + k], j1 = off[(size_t)b * (K + 1) + k + 1];
-  const int c0 = j0 / cr, c1 = (j1 - 1) / cr;
+  const int c0 = j0 / cr, c1 = n == 0 ? c0 : (j1 - 1) / cr;
   const float fn = (float)n;
-  if (c0 == c1) {
+  if (n == 0) {
+    for (int d = t; d < D4; d += 256) {
+      const float4 v = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = v;
+      row4[d] = v;
+    }
+  } else if (c0 == c1) {
     for (int d = t; d < D4; d += 256) {
       const float4 s = reinterpret_cast<const float4*>(sums + rowoff)[d];
-      reinterpret_cast<float4*>(C_out + rowoff)[d] =
-          make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
+      const float4 m = make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
+      row4[d] = m;
     }
-    return;
-  }
-  const int slot = (D4 >= 256) ? 0 : t / D4;
-  for (int d0 = 0; d0 < D4; d0 += 256) {
-    const int d = d0 + (D4 >= 256 ? t : t % D4);
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (slot < slots && d < D4) {
-      for (int c = c0 + slot; c <= c1; c += slots) {
-        const int which = (c == c0 && j0 > c * cr) ? 1 : 0;
-        const float4 v = reinterpret_cast<const float4*>(
-            carry + (((size_t)b * nred + c) * 2 + which) * D)[d];
-        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  } else {
+    const int slot = (D4 >= 256) ? 0 : t / D4;
+    for (int d0 = 0; d0 < D4; d0 += 256) {
+      const int d = d0 + (D4 >= 256 ? t : t % D4);
+      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (slot < slots && d < D4) {
+        for (int c = c0 + slot; c <= c1; c += slots) {
+          const int which = (c == c0 && j0 > c * cr) ? 1 : 0;
+          const float4 v = reinterpret_cast<const float4*>(
+              carry + (((size_t)b * nred + c) * 2 + which) * D)[d];
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+      }
+      __syncthreads();
+      part[t] = s;
+      __syncthreads();
+      if (slot == 0 && d < D4) {
+        for (int u = 1; u < slots; ++u) {
+          const float4 v = part[u * D4 + (t % D4)];
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        const float4 m = make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
+        reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
+        row4[d] = m;
       }
     }
-    __syncthreads();
-    part[t] = s;
-    __syncthreads();
-    if (slot == 0 && d < D4) {
-      for (int u = 1; u < slots; ++u) {
-        const float4 v = part[u * D4 + (t % D4)];
-        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-      }
-      reinterpret_cast<float4*>(C_out + rowoff)[d] =
-          make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
-    }
   }
+  __syncthreads();
+  next_step_tail(nx, row, b, k, D, t, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -561,9 +597,11 @@ __global__ __launch_bounds__(1024) void smallk_partials_kernel(
 // cluster keeps its previous centroid.
 __global__ __launch_bounds__(256) void smallk_combine_kernel(
     const float* __restrict__ partial, const int32_t* __restrict__ pcount, const float* C_prev,
-    int K, int D, int nch, float* C_out, int32_t* __restrict__ counts) {
+    int K, int D, int nch, float* C_out, int32_t* __restrict__ counts, NextStep nx) {
   __shared__ int wsum[4];
   __shared__ float4 part[256];
+  __shared__ __attribute__((aligned(16))) float row[MAX_D];
+  __shared__ double red[256];
   const int k = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   int n = 0;
   for (int c = t; c < nch; c += 256) n += pcount[((size_t)b * nch + c) * K + k];
@@ -572,37 +610,44 @@ __global__ __launch_bounds__(256) void smallk_combine_kernel(
   if (t == 0) counts[(size_t)b * K + k] = total;
   const int D4 = D / 4;
   const size_t rowoff = ((size_t)b * K + k) * D;
+  float4* row4 = reinterpret_cast<float4*>(row);
   if (total == 0) {
-    for (int d = t; d < D4; d += 256)
-      reinterpret_cast<float4*>(C_out + rowoff)[d] = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
-    return;
-  }
-  const float fn = (float)total;
-  const int slots = D4 >= 256 ? 1 : 256 / D4;
-  const int slot = D4 >= 256 ? 0 : t / D4;
-  const float4* pb = reinterpret_cast<const float4*>(partial + ((size_t)b * nch * K + k) * D);
-  const size_t cstride = (size_t)K * D4;  // float4s from one chunk's row k to the next chunk's
-  for (int d0 = 0; d0 < D4; d0 += 256) {
-    const int d = d0 + (D4 >= 256 ? t : t % D4);
-    float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (slot < slots && d < D4) {
-      for (int c = slot; c < nch; c += slots) {
-        const float4 v = pb[c * cstride + d];
-        sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
+    for (int d = t; d < D4; d += 256) {
+      const float4 v = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = v;
+      row4[d] = v;
+    }
+  } else {
+    const float fn = (float)total;
+    const int slots = D4 >= 256 ? 1 : 256 / D4;
+    const int slot = D4 >= 256 ? 0 : t / D4;
+    const float4* pb = reinterpret_cast<const float4*>(partial + ((size_t)b * nch * K + k) * D);
+    const size_t cstride = (size_t)K * D4;  // float4s from one chunk's row k to the next chunk's
+    for (int d0 = 0; d0 < D4; d0 += 256) {
+      const int d = d0 + (D4 >= 256 ? t : t % D4);
+      float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (slot < slots && d < D4) {
+        for (int c = slot; c < nch; c += slots) {
+          const float4 v = pb[c * cstride + d];
+          sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
+        }
+      }
+      __syncthreads();
+      part[t] = sacc;
+      __syncthreads();
+      if (slot == 0 && d < D4) {
+        for (int u = 1; u < slots; ++u) {
+          const float4 v = part[u * D4 + (t % D4)];
+          sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
+        }
+        const float4 m = make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
+        reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
+        row4[d] = m;
       }
     }
-    __syncthreads();
-    part[t] = sacc;
-    __syncthreads();
-    if (slot == 0 && d < D4) {
-      for (int u = 1; u < slots; ++u) {
-        const float4 v = part[u * D4 + (t % D4)];
-        sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
-      }
-      reinterpret_cast<float4*>(C_out + rowoff)[d] =
-          make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
-    }
   }
+  __syncthreads();
+  next_step_tail(nx, row, b, k, D, t, red);
 }
 
 template <int DT, int LPR, int CPLR>
@@ -642,7 +687,7 @@ static hipError_t launch_smallk_dt(const void* X, const int32_t* idx, const Work
 static hipError_t launch_update_smallk(const void* X, int dt, const int32_t* idx,
                                        const float* C_prev, const Workspace& w, int64_t B,
                                        int64_t N, int64_t D, int64_t K, float* C_out,
-                                       int32_t* counts, hipStream_t s) {
+                                       int32_t* counts, const NextStep& nx, hipStream_t s) {
   int dbits = 0;
   while ((1ll << dbits) < K) ++dbits;
   hipError_t e;
@@ -650,9 +695,7 @@ static hipError_t launch_update_smallk(const void* X, int dt, const int32_t* idx
   else if (dt == DT_F16) e = launch_smallk_dt<DT_F16>(X, idx, w, B, N, D, K, dbits, s);
   else e = launch_smallk_dt<DT_F32>(X, idx, w, B, N, D, K, dbits, s);
   if (e != hipSuccess) return e;
-  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
-      w.partial, w.pcount, C_prev, (int)K, (int)D, (int)w.n_sk_chunks, C_out, counts);
-  return hipGetLastError();
+  return launch_combine(w, w.n_sk_chunks, C_prev, B, K, D, C_out, counts, nx, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -713,23 +756,24 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
 }
 
 hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
-                          int64_t K, int64_t D, float* C_out, int32_t* counts, hipStream_t s) {
+                          int64_t K, int64_t D, float* C_out, int32_t* counts,
+                          const NextStep& nx, hipStream_t s) {
   smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
-      w.partial, w.pcount, C_prev, (int)K, (int)D, (int)nch, C_out, counts);
+      w.partial, w.pcount, C_prev, (int)K, (int)D, (int)nch, C_out, counts, nx);
   return hipGetLastError();
 }
 
 hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float* C_prev,
                          const Workspace& w, int64_t B, int64_t N, int64_t D, int64_t K,
-                         float* C_out, int32_t* counts, hipStream_t s) {
+                         float* C_out, int32_t* counts, const NextStep& nx, hipStream_t s) {
   if (sums_ok(dt, D, K)) {
     const hipError_t e = launch_sums(X, dt, w, B, N, D, K, SUMS_ONLY, const_cast<int32_t*>(idx),
                                      nullptr, s);
     if (e != hipSuccess) return e;
-    return launch_combine(w, w.n_sk_chunks, C_prev, B, K, D, C_out, counts, s);
+    return launch_combine(w, w.n_sk_chunks, C_prev, B, K, D, C_out, counts, nx, s);
   }
   if (smallk_ok(dt, D, K))
-    return launch_update_smallk(X, dt, idx, C_prev, w, B, N, D, K, C_out, counts, s);
+    return launch_update_smallk(X, dt, idx, C_prev, w, B, N, D, K, C_out, counts, nx, s);
   hipError_t e;
   const int nch = (int)w.n_sort_chunks;
   int passes, d1, d2;
@@ -767,10 +811,9 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
   else if (dt == DT_F16) e = launch_segreduce_dt<DT_F16>(X, w, B, N, D, K, s);
   else e = launch_segreduce_dt<DT_F32>(X, w, B, N, D, K, s);
   if (e != hipSuccess) return e;
-  const size_t part_bytes = 256 * sizeof(float4);
-  finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, part_bytes, s>>>(
+  finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
       w.sums, w.carry, counts, w.off, C_prev, (int)K, (int)D, (int)w.n_red_chunks, (int)w.red_cr,
-      C_out);
+      C_out, nx);
   return hipGetLastError();
 }
 
