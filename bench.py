@@ -38,14 +38,17 @@ def kernel_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def stored_traffic():
-    """Measured HBM bytes per assignment launch, if taken on the current kernel source."""
+def stored_traffic(workload: str):
+    """Measured HBM bytes per assignment launch, if taken on this workload and
+    the current kernel source."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    return rec.get("bytes_per_launch") if rec.get("kernel_sha256_16") == kernel_hash() else None
+    if rec.get("workload") != workload or rec.get("kernel_sha256_16") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def cpu_baseline(w, sample_rows: int):
@@ -233,7 +236,7 @@ def main():
                    "centroid_dtype": "f32", "iters_per_step": 1},
         "roofline": {"bound": "mfma", "kernel": "assign", "achieved": assign_tflops,
                      "peak": peak, "unit": "TFLOP/s",
-                     "frac": assign_tflops / peak, "traffic": stored_traffic()},
+                     "frac": assign_tflops / peak, "traffic": stored_traffic(w.name)},
         "update": {"ms": update_ms, "algorithmic_bytes": upd_bytes, "GB/s": upd_gbs,
                    "hbm_frac": upd_gbs / PEAK_HBM_GBS},
         "assign_ms": assign_ms,

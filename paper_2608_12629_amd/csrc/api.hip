@@ -21,9 +21,12 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   if (assign_tiled(dt, D)) {
     w.n_assign_blocks = (N + 255) / 256;  // the decode kernel's blocks
   } else {
-    const int64_t ppb = assign_points_per_block(dt, D);
+    const int64_t ppb = assign_points_per_block(dt, D, B * N);
     w.n_assign_blocks = (N + ppb - 1) / ppb;
   }
+  // fp32 workgroups shrink to 128 points for small problems: size the
+  // partials for that, so the workspace never shrinks as N grows
+  const int64_t nparts = dt == DT_F32 ? (N + 127) / 128 : w.n_assign_blocks;
   w.n_sort_chunks = (N + RADIX_CHUNK - 1) / RADIX_CHUNK;
   w.red_cr = red_slice(B, N);
   w.n_red_chunks = (N + w.red_cr - 1) / w.red_cr;
@@ -37,7 +40,7 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   w.Kp = kpad_for(dt, D, K);
   w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
   w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
-  w.objpart = (double*)take((size_t)(B * w.n_assign_blocks) * 8);
+  w.objpart = (double*)take((size_t)(B * nparts) * 8);
   w.rhist = (int32_t*)take((size_t)(B * RADIX_MAX_R * w.n_sort_chunks) * 4);
   w.rbin = (int32_t*)take((size_t)B * RADIX_MAX_R * 4);
   w.rtotal = (int32_t*)take((size_t)B * 4);

@@ -201,14 +201,20 @@ hipError_t launch_prep(const float* C, int dt, int64_t B, int64_t K, int64_t Kp,
   return hipGetLastError();
 }
 
+// NSUB as assign_nsub32 gives it: the D-dependent value, or 2 for small problems.
 template <int DT, int CPL>
 static hipError_t launch_resident(const void* X, const Workspace& w, int64_t B, int64_t N,
                                   int64_t K, int32_t* idx, float* min_dist, hipStream_t s) {
-  constexpr int NSUB = CPL <= 4 ? 8 : (CPL <= 8 ? 4 : 2);  // must agree with assign_nsub32
+  constexpr int BASE = CPL <= 4 ? 8 : (CPL <= 8 ? 4 : 2);
   const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
-  assign_resident_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
-      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)K, (int)w.Kp, idx, min_dist,
-      w.objpart);
+  const uint4* Xv = (const uint4*)X;
+  const uint4* ch = (const uint4*)w.chat;
+  if (assign_nsub32(16 * CPL, B * N) == BASE)
+    assign_resident_kernel<DT, CPL, BASE><<<grid, block, 0, s>>>(
+        Xv, ch, w.cinit, (int)N, (int)K, (int)w.Kp, idx, min_dist, w.objpart);
+  else
+    assign_resident_kernel<DT, CPL, 2><<<grid, block, 0, s>>>(
+        Xv, ch, w.cinit, (int)N, (int)K, (int)w.Kp, idx, min_dist, w.objpart);
   return hipGetLastError();
 }
 

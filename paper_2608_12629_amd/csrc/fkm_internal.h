@@ -87,12 +87,17 @@ inline bool row_bytes_ok(int dt, int64_t D) {
 // Points per assignment workgroup.  16-bit storage: 32x32x16 MFMA tiles, 4
 // waves x NSUB x 32 points, NSUB by the D / 16 chunks a lane holds (4 up to 4
 // chunks, 2 up to 8, else 1).  fp32: 16x16x4 MFMA tiles, 4 waves x NSUB x 16
-// points (NSUB = 8 up to D = 64, 4 up to 128, else 2).
+// points (NSUB = 8 up to D = 64, 4 up to 128, else 2), and 2 when B x N
+// points would give fewer than 512 workgroups (two per CU) at the larger
+// NSUB: a small problem then fills the chip with smaller workgroups.
 inline int assign_nsub16(int64_t D) { return D <= 64 ? 4 : (D <= 128 ? 2 : 1); }
-inline int assign_nsub32(int64_t D) { return D <= 64 ? 8 : (D <= 128 ? 4 : 2); }
-inline int64_t assign_points_per_block(int dt, int64_t D) {
+inline int assign_nsub32(int64_t D, int64_t BN) {
+  const int base = D <= 64 ? 8 : (D <= 128 ? 4 : 2);
+  return base > 2 && BN < (int64_t)512 * 64 * base ? 2 : base;
+}
+inline int64_t assign_points_per_block(int dt, int64_t D, int64_t BN) {
   if (dt != DT_F32) return 4 * 32 * assign_nsub16(D);
-  return 4 * 16 * assign_nsub32(D);
+  return 4 * 16 * assign_nsub32(D, BN);
 }
 
 // The resident-X assignment kernels hold a point in registers: rows up to

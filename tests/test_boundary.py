@@ -69,6 +69,13 @@ def test_workspace_bytes(lib):
             cur = ws(1, N, 128, K)
             assert cur >= prev
             prev = cur
+    # fp32 workgroups shrink for small problems (more of them): still monotone
+    for D, K in ((64, 256), (128, 4096)):
+        prev = 0
+        for N in (1, 65536, 65537, 131071, 131072, 262143, 262144, 1 << 20):
+            cur = ws(1, N, D, K, F32)
+            assert cur >= prev, (D, K, N)
+            prev = cur
     for K in (1, 7, 64, 1000, 4096, 32768, 65536):
         assert ws(1, 65536, 64, K) > 0
     assert ws(4, 1000, 64, 10) >= ws(1, 1000, 64, 10)
