@@ -2,11 +2,12 @@
 // D > 256, a multiple of 32), where a point no longer fits in registers.
 //
 // The distance contraction is tiled like a GEMM.  A workgroup owns 256 points
-// and up to TILED_CBG consecutive 256-centroid blocks; its four waves split
-// each 256 x 256 block 2 x 2, so a wave owns 128 points x 128 centroids: 4 x 4
-// 32x32x16 MFMA tiles, 16 independent accumulators (one wave per SIMD).  Per
-// 16-dimension step a wave reads 4 centroid and 4 point fragments from LDS
-// for 16 MFMAs.
+// and up to TILED_CBG consecutive 256-centroid blocks; its eight waves split
+// each 256 x 256 block 2 x 4, so a wave owns 128 points x 64 centroids: 4 x 2
+// 32x32x16 MFMA tiles, 8 independent accumulators, and two waves share each
+// SIMD (one wave of 4 x 4 tiles per SIMD left every LDS and barrier latency
+// exposed).  Per 16-dimension step a wave reads 2 centroid and 4 point
+// fragments from LDS for 8 MFMAs.
 //
 // Staging.  D streams through LDS in 32-dimension stages holding both
 // operands and the block's scores.  Each stage goes from L2 straight into LDS
@@ -51,17 +52,21 @@ namespace fkm {
 
 namespace {
 
+constexpr int TT = 512;                  // threads per workgroup (8 waves)
 constexpr int BP = TILED_BP;             // points per workgroup
 constexpr int BC = TILED_BC;             // centroids per block
 constexpr int DC = 32;                   // dimensions per LDS stage
 constexpr int CPS = DC * 2 / 16;         // 16-byte chunks of a row in one stage (4)
 constexpr int XB = BP * CPS * 16;        // bytes of point chunks per stage
 constexpr int CB = BC * CPS * 16;        // bytes of centroid chunks per stage
-constexpr int STAGE = XB + CB + BC * 4;  // + the block's scores
-constexpr int LX = BP * CPS / 256;       // point chunks per thread per stage
-constexpr int LC = BC * CPS / 256;       // centroid chunks per thread per stage
+// + the block's scores, and a second copy that the upper four waves load so
+// that every wave issues the same number of loads
+constexpr int STAGE = XB + CB + 2 * BC * 4;
+constexpr int LX = BP * CPS / TT;        // point chunks per thread per stage
+constexpr int LC = BC * CPS / TT;        // centroid chunks per thread per stage
 constexpr int LOADS = LX + LC + 1;       // loads per thread per stage (+ one score)
-static_assert(BP == 256 && BC == 256, "2 x 2 waves of 128 x 128");
+constexpr int RSTEP = TT / CPS;          // rows between a thread's loads (128)
+static_assert(BP == 256 && BC == 256, "2 x 4 waves of 128 x 64");
 static_assert(2 * LOADS <= 63, "vmcnt counts at most 63 loads");
 static_assert(CB <= TILED_ZERO_BYTES, "a padding stage's centroid chunks fit the zero area");
 
@@ -107,7 +112,7 @@ struct TiledCtx {
   const char* zero;    // CB zeroed bytes: the centroid chunks of a padding stage
   uint32_t xoff;       // lane byte offset of its first point chunk (row clamped to the last point)
   uint32_t coff;       // lane byte offset of its first centroid chunk
-  uint32_t rows64;     // bytes of 64 rows
+  uint32_t rowsstep;   // bytes of RSTEP rows
   int last;            // last valid row of the point block
   int nds;             // stages of 32 dimensions per block (D / 32)
   int ndsv;            // stages per block, padded to a multiple of 4
@@ -115,7 +120,7 @@ struct TiledCtx {
 };
 
 // Stage s = (block s / ndsv, dimensions 32 (s % ndsv) ..): start its loads into buf.
-// Load u of a thread covers slot tid + 256 u: row tid / 4 + 64 u, chunk
+// Load u of a thread covers slot tid + 512 u: row tid / 4 + 128 u, chunk
 // (tid % 4) ^ swz(row) (swz has period 16, so the chunk order repeats).
 __device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf) {
   const int g = s / c.ndsv, dv = s % c.ndsv, ds = min(dv, c.nds - 1);
@@ -125,53 +130,58 @@ __device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf)
 #pragma unroll
   for (int u = 0; u < LX; ++u) {
     // rows past the last point reload the last point (their results are dropped)
-    const uint32_t off = (c.tid >> 2) + 64 * u <= c.last
-                             ? c.xoff + u * c.rows64
+    const uint32_t off = (c.tid >> 2) + RSTEP * u <= c.last
+                             ? c.xoff + u * c.rowsstep
                              : (uint32_t)((c.last * c.RC + ((c.tid & 3) ^ swz(c.tid >> 2))) * 16);
     __builtin_amdgcn_global_load_lds((global_void*)(xb + off),
-                                     (lds_void*)(buf + (u * 256 + wave * 64) * 16), 16, 0, 0);
+                                     (lds_void*)(buf + (u * TT + wave * 64) * 16), 16, 0, 0);
   }
   const int krow = (c.cb0 + g) * BC;
   const char* cbp = c.chat + ((size_t)krow * c.RC + ds * CPS) * 16;
 #pragma unroll
   for (int u = 0; u < LC; ++u) {
-    const char* src = pad ? c.zero + (u * 256 + c.tid) * 16 : cbp + c.coff + u * c.rows64;
+    const char* src = pad ? c.zero + (u * TT + c.tid) * 16 : cbp + c.coff + u * c.rowsstep;
     __builtin_amdgcn_global_load_lds((global_void*)src,
-                                     (lds_void*)(buf + XB + (u * 256 + wave * 64) * 16), 16, 0, 0);
+                                     (lds_void*)(buf + XB + (u * TT + wave * 64) * 16), 16, 0, 0);
   }
   // the block's scores ride with every stage, so every stage issues LOADS loads
-  __builtin_amdgcn_global_load_lds((global_void*)(c.cinit + krow + c.tid),
+  // (waves 4 .. 7 load a second copy, never read)
+  __builtin_amdgcn_global_load_lds((global_void*)(c.cinit + krow + (c.tid & (BC - 1))),
                                    (lds_void*)(buf + XB + CB + wave * 256), 4, 0, 0);
 }
 
 // Fragments of one 16-dimension step: 4 centroid tiles and 4 point tiles.
+constexpr int TCW = 2;  // 32-centroid tiles per wave
 struct TiledFrag {
-  uint4 a[4], b[4];
+  uint4 a[TCW], b[4];
 };
 
 __device__ __forceinline__ void tiled_read(TiledFrag& f, char* buf, int lo, int wp, int wc) {
 #pragma unroll
-  for (int tc = 0; tc < 4; ++tc) f.a[tc] = lds_at<uint4>(buf, XB + (wc * 128 + tc * 32) * 64 + lo);
+  for (int tc = 0; tc < TCW; ++tc)
+    f.a[tc] = lds_at<uint4>(buf, XB + (wc * 32 * TCW + tc * 32) * 64 + lo);
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp) f.b[tp] = lds_at<uint4>(buf, (wp * 128 + tp * 32) * 64 + lo);
 }
 
 template <int DT>
-__device__ __forceinline__ void tiled_mfma(f32x16 (&acc)[4][4], const TiledFrag& f) {
+__device__ __forceinline__ void tiled_mfma(f32x16 (&acc)[4][TCW], const TiledFrag& f) {
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp)
 #pragma unroll
-    for (int tc = 0; tc < 4; ++tc) acc[tp][tc] = mfma32_chunk<DT>(f.a[tc], f.b[tp], acc[tp][tc]);
+    for (int tc = 0; tc < TCW; ++tc) acc[tp][tc] = mfma32_chunk<DT>(f.a[tc], f.b[tp], acc[tp][tc]);
 }
 
 // A new block: every accumulator starts at its centroid's -|c^|^2/2 - Q.
-__device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][4], char* buf, int wc, int h, float Q) {
+__device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][TCW], char* buf, int wc, int h,
+                                           float Q) {
 #pragma unroll
-  for (int tc = 0; tc < 4; ++tc) {
+  for (int tc = 0; tc < TCW; ++tc) {
     f32x16 cin;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const f32x4 v = lds_at<f32x4>(buf, XB + CB + (wc * 128 + tc * 32 + 8 * q + 4 * h) * 4);
+      const f32x4 v =
+          lds_at<f32x4>(buf, XB + CB + (wc * 32 * TCW + tc * 32 + 8 * q + 4 * h) * 4);
       cin[4 * q + 0] = v[0] - Q;
       cin[4 * q + 1] = v[1] - Q;
       cin[4 * q + 2] = v[2] - Q;
@@ -189,7 +199,7 @@ __device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][4], char* buf, int w
 // second step's MFMAs.  TAIL: stages past the end may follow.
 template <int DT, bool TAIL>
 __device__ __forceinline__ void tiled_stage(const TiledCtx& c, int s, char* cur, char* nxt,
-                                            char* ahead, f32x16 (&acc)[4][4], TiledFrag& f0,
+                                            char* ahead, f32x16 (&acc)[4][TCW], TiledFrag& f0,
                                             TiledFrag& f1) {
   tiled_read(f1, cur, c.loff1, c.wp, c.wc);
   tiled_mfma<DT>(acc, f0);
@@ -203,7 +213,7 @@ __device__ __forceinline__ void tiled_stage(const TiledCtx& c, int s, char* cur,
 // Four stages; stage s0 is in buffer 0.
 template <int DT, bool TAIL>
 __device__ __forceinline__ void tiled_quad(const TiledCtx& c, int s0, char* b0, char* b1, char* b2,
-                                           char* b3, f32x16 (&acc)[4][4], TiledFrag& f0,
+                                           char* b3, f32x16 (&acc)[4][TCW], TiledFrag& f0,
                                            TiledFrag& f1) {
   tiled_stage<DT, TAIL>(c, s0, b0, b1, b3, acc, f0, f1);
   tiled_stage<DT, TAIL>(c, s0 + 1, b1, b2, b0, acc, f0, f1);
@@ -213,12 +223,12 @@ __device__ __forceinline__ void tiled_quad(const TiledCtx& c, int s0, char* b0, 
 
 // The block is complete: packed-key arg-max of each tile into the running
 // (best, code) of each point tile; tiles are visited in increasing index order.
-__device__ __forceinline__ void tiled_epilogue(const f32x16 (&acc)[4][4], float (&best)[4],
+__device__ __forceinline__ void tiled_epilogue(const f32x16 (&acc)[4][TCW], float (&best)[4],
                                                uint32_t (&code)[4], uint32_t tile0) {
 #pragma unroll
   for (int tp = 0; tp < 4; ++tp)
 #pragma unroll
-    for (int tc = 0; tc < 4; ++tc) {
+    for (int tc = 0; tc < TCW; ++tc) {
       float k[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j)
@@ -241,7 +251,7 @@ __device__ __forceinline__ void tiled_epilogue(const f32x16 (&acc)[4][4], float 
 }  // namespace
 
 template <int DT>
-__global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
+__global__ __launch_bounds__(TT, 1) void assign_tiled_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
     const float* __restrict__ xnorm, const uint4* __restrict__ zero, int N, int D, int Kp, int npb,
     int ncbg, uint64_t* __restrict__ keys) {
@@ -249,13 +259,13 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   __shared__ __attribute__((aligned(16))) char buf1[STAGE];
   __shared__ __attribute__((aligned(16))) char buf2[STAGE];
   __shared__ __attribute__((aligned(16))) char buf3[STAGE];
-  __shared__ float lds_q[4];
+  __shared__ float lds_q[8];
 
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
-  const int wp = wave & 1, wc = wave >> 1;
+  const int wp = wave & 1, wc = wave >> 1;  // point half, centroid quarter
   const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
   const int sup = j / (8 * ncbg), cbg = (j / 8) % ncbg;
   const int pb = (sup * 8 + xcd) * 8 + (j & 7);
@@ -275,7 +285,7 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   c.last = min(BP, N - p0) - 1;
   c.xoff = (uint32_t)((min(tid >> 2, c.last) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
   c.coff = (uint32_t)(((tid >> 2) * RC + ((tid & 3) ^ swz(tid >> 2))) * 16);
-  c.rows64 = (uint32_t)(64 * RC * 16);
+  c.rowsstep = (uint32_t)(RSTEP * RC * 16);
   c.nds = nds;
   c.ndsv = ndsv;
   c.cb0 = cb0;
@@ -288,8 +298,8 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   c.wp = wp;
   c.wc = wc;
 
-  // Q of the point block
-  float xm = tid <= c.last ? xnorm[(size_t)b * N + p0 + tid] : 0.f;
+  // Q of the point block (waves 0 .. 3 hold its 256 norms)
+  float xm = tid < BP && tid <= c.last ? xnorm[(size_t)b * N + p0 + tid] : 0.f;
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) xm = __builtin_fmaxf(xm, __shfl_xor(xm, m));
   if (lane == 0) lds_q[wave] = xm;
@@ -305,7 +315,7 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
   const float Q =
       block_q(__builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])));
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][TCW];
   float best[4];
   uint32_t code[4];
 #pragma unroll
@@ -323,13 +333,14 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
     for (int q = 0; q < full; ++q)
       tiled_quad<DT, false>(c, s0 + 4 * q, buf0, buf1, buf2, buf3, acc, f0, f1);
     if (full < nq) tiled_quad<DT, true>(c, s0 + 4 * full, buf0, buf1, buf2, buf3, acc, f0, f1);
-    tiled_epilogue(acc, best, code, (uint32_t)((cb0 + g) * (BC / 32) + wc * 4));
+    tiled_epilogue(acc, best, code, (uint32_t)((cb0 + g) * (BC / 32) + wc * TCW));
   }
 
-  // merge the two row halves of each point, then the two centroid halves of
-  // the workgroup (waves wc = 1 hand theirs over through LDS)
+  // merge the two row halves of each point, then the four centroid quarters
+  // of the workgroup (waves wc = 1 .. 3 hand theirs over through LDS; wave
+  // wc = 0 takes them in quarter order)
   float* mv = reinterpret_cast<float*>(buf0);
-  int* mi = reinterpret_cast<int*>(buf0 + BP * 4);
+  int* mi = reinterpret_cast<int*>(buf0 + 4 * BP * 4);
   float v[4];
   int ix[4];
 #pragma unroll
@@ -342,11 +353,11 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
     v[tp] = take ? vo : best[tp];
     ix[tp] = take ? io : i;
   }
-  if (wc == 1 && h == 0) {
+  if (wc != 0 && h == 0) {
 #pragma unroll
     for (int tp = 0; tp < 4; ++tp) {
-      mv[wp * 128 + tp * 32 + n] = v[tp];
-      mi[wp * 128 + tp * 32 + n] = ix[tp];
+      mv[wc * BP + wp * 128 + tp * 32 + n] = v[tp];
+      mi[wc * BP + wp * 128 + tp * 32 + n] = ix[tp];
     }
   }
   __syncthreads();
@@ -354,11 +365,16 @@ __global__ __launch_bounds__(256, 1) void assign_tiled_kernel(
 #pragma unroll
     for (int tp = 0; tp < 4; ++tp) {
       const int r = wp * 128 + tp * 32 + n;
-      const float vo = mv[r];
-      const int io = mi[r];
-      const bool take = (vo > v[tp]) || (vo == v[tp] && io < ix[tp]);
-      const float vv = take ? vo : v[tp];
-      const int ii = take ? io : ix[tp];
+      float vv = v[tp];
+      int ii = ix[tp];
+#pragma unroll
+      for (int q = 1; q < 4; ++q) {
+        const float vo = mv[q * BP + r];
+        const int io = mi[q * BP + r];
+        const bool take = (vo > vv) || (vo == vv && io < ii);
+        vv = take ? vo : vv;
+        ii = take ? io : ii;
+      }
       if (r <= c.last) {
         const uint64_t key = ((uint64_t)ordered(vv) << 32) | (uint64_t)(0xffffffffu - (uint32_t)ii);
         atomicMax((unsigned long long*)&keys[(size_t)b * N + p0 + r], (unsigned long long)key);
@@ -451,11 +467,11 @@ hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_
   const int npb64 = (npb + 63) / 64 * 64;  // whole super-tiles on every XCD
   const dim3 grid((unsigned)(npb64 * ncbg), (unsigned)B);
   if (dt == DT_BF16)
-    assign_tiled_kernel<DT_BF16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
+    assign_tiled_kernel<DT_BF16><<<grid, TT, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
                                                       w.cinit, w.xnorm, (const uint4*)(w.keys + nz),
                                                       (int)N, (int)D, (int)w.Kp, npb, ncbg, w.keys);
   else
-    assign_tiled_kernel<DT_F16><<<grid, 256, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
+    assign_tiled_kernel<DT_F16><<<grid, TT, 0, s>>>((const uint4*)X, (const uint4*)w.chat,
                                                      w.cinit, w.xnorm, (const uint4*)(w.keys + nz),
                                                      (int)N, (int)D, (int)w.Kp, npb, ncbg, w.keys);
   if ((e = hipGetLastError()) != hipSuccess) return e;
