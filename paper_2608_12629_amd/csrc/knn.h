@@ -116,12 +116,33 @@ __device__ __forceinline__ float knn_pick(const f32x16& acc, int j) {
   return s;
 }
 
+// The top-k update of one tile: the scores that beat the lane's KMAX-th best
+// are marked, and while any lane has a mark left, each lane inserts its
+// lowest marked score (so rows still enter in index order).
+template <int KMAX>
+__device__ __forceinline__ void knn_update(const f32x16& acc, int base, float (&v)[KMAX],
+                                           int (&ix)[KMAX]) {
+  uint32_t mark = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) mark |= (acc[j] > v[KMAX - 1] ? 1u : 0u) << j;
+  while (__ballot(mark != 0)) {
+    if (mark != 0) {
+      const int j = __builtin_ctz(mark);
+      mark &= mark - 1;
+      const float sc = knn_pick(acc, j);
+      // an earlier insertion may have raised the bar
+      if (sc > v[KMAX - 1]) knn_insert<KMAX>(v, ix, sc, base + 8 * (j >> 2) + (j & 3));
+    }
+  }
+}
+
 // One stage in `cur`: start the next stage into `nxt` (a different LDS array,
 // so no read of `cur` waits for it), then per 32-row tile the MFMAs and the
-// top-k update: the scores that beat the lane's KMAX-th best are marked, and
-// while any lane has a mark left, each lane inserts its lowest marked score
-// (so rows still enter in index order).  Store the next stage's scores, wait
-// for its loads and sync.
+// top-k update; with 32-entry lists (one wave per SIMD, nothing else to hide
+// behind) the MFMAs of the next tile run beside this tile's update (two
+// accumulator sets: the matrix pipe and the vector ALU overlap only within a
+// wave's own instruction stream).  Store the next stage's scores, wait for
+// its loads and sync.
 template <int DT, int CPL, int KMAX, int LOADS>
 __device__ __forceinline__ void knn_stage(int st, int nst, char* cur, char* nxt,
                                           const PipeOffsets<CPL, LOADS>& o,
@@ -132,21 +153,21 @@ __device__ __forceinline__ void knn_stage(int st, int nst, char* cur, char* nxt,
   const bool more = st + 1 < nst;
   float nn = 0.f;
   if (more) nn = pipe_issue_stage<CPL, LOADS>(chat4, cinit, st + 1, tid, o, nxt);
-  for (int tile = 0; tile < L::TILES; ++tile) {
-    f32x16 acc;
-    knn_mfma_tile<DT, CPL, LOADS>(acc, xr, cur, o, tile);
-    uint32_t mark = 0;
+  if constexpr (KMAX > 16) {
+    f32x16 acc[2];
+    knn_mfma_tile<DT, CPL, LOADS>(acc[0], xr, cur, o, 0);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) mark |= (acc[j] > v[KMAX - 1] ? 1u : 0u) << j;
-    const int base = (st * L::TILES + tile) * 32 + 4 * h;
-    while (__ballot(mark != 0)) {
-      if (mark != 0) {
-        const int j = __builtin_ctz(mark);
-        mark &= mark - 1;
-        const float sc = knn_pick(acc, j);
-        // an earlier insertion may have raised the bar
-        if (sc > v[KMAX - 1]) knn_insert<KMAX>(v, ix, sc, base + 8 * (j >> 2) + (j & 3));
-      }
+    for (int tile = 0; tile < L::TILES; ++tile) {
+      if (tile + 1 < L::TILES)
+        knn_mfma_tile<DT, CPL, LOADS>(acc[(tile + 1) & 1], xr, cur, o, tile + 1);
+      knn_update<KMAX>(acc[tile & 1], (st * L::TILES + tile) * 32 + 4 * h, v, ix);
+    }
+  } else {
+    // within 256 registers the second accumulator set costs spills
+    for (int tile = 0; tile < L::TILES; ++tile) {
+      f32x16 acc;
+      knn_mfma_tile<DT, CPL, LOADS>(acc, xr, cur, o, tile);
+      knn_update<KMAX>(acc, (st * L::TILES + tile) * 32 + 4 * h, v, ix);
     }
   }
   if (more) lds_at<float>(nxt, o.n_store, 0) = nn;
