@@ -20,6 +20,10 @@
  *   squared norm of the rounded centroid, so each distance is the distance to
  *   that rounded centroid, accumulated in fp32.
  * - Indices are int32 and local to an instance: idx[b, i] is in [0, K).
+ * - Points and centroids must be finite.  (Non-finite values give unspecified
+ *   results; with small K the sums are formed by multiplying every point by a
+ *   0/1 membership, so one infinite coordinate turns that dimension of every
+ *   cluster's mean into NaN.)
  * - Ties go to the lowest centroid index.  An empty cluster keeps its previous
  *   centroid (and reports count 0).
  * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
