@@ -134,3 +134,37 @@ def test_knn_self_query(km):
     dup_ok = (Rd[0][first.cuda()] == Rd[0]).all(-1).cpu()
     assert bool(((first == own) | dup_ok).all())
     assert (gd[..., 0] <= 1e-3 * scale).all()
+
+
+def test_knn_full_size_sampled(km, oracle):
+    """The bench's search (262,144 queries against 1,048,576 rows, D = 128, k = 10,
+    bf16, the same seeded blob recipe) in its launch configuration; 24 sampled
+    queries checked against the oracle's 26 nearest rows with the tolerance of
+    the small cases, distances of returned rows recomputed exactly."""
+    M, N, D, k = 262144, 1 << 20, 128, 10
+    g = torch.Generator().manual_seed(7)
+    centres = torch.rand((N // 64, D), generator=g) * 2 - 1
+    R = (centres[torch.randint(0, N // 64, (N,), generator=g)] + 0.1 * torch.randn((N, D), generator=g))
+    Q = (centres[torch.randint(0, N // 64, (M,), generator=g)] + 0.1 * torch.randn((M, D), generator=g))
+    R, Q = R.to(torch.bfloat16), Q.to(torch.bfloat16)
+    say(f"[knn full] M={M} N={N} D={D} k={k}")
+    gi, gd = km.kmeans_knn(Q.cuda(), R.cuda(), k)
+    torch.cuda.synchronize()
+    rows = np.random.default_rng(11).choice(M, 24, replace=False)
+    Qs = Q[None, rows]
+    oi, od, _ = oracle.knn(raw(Qs), raw(R[None]), "bf16", k + 16)
+    q64 = oracle.widen(raw(Qs), "bf16")[0]
+    r64 = oracle.widen(raw(R[None]), "bf16")[0]
+    gi_s, gd_s = gi[0].cpu().numpy()[rows], gd[0].cpu().numpy()[rows].astype(np.float64)
+    for m in range(len(rows)):
+        S = gi_s[m]
+        assert len(set(S.tolist())) == k and S.min() >= 0 and S.max() < N
+        d_ret = ((r64[S] - q64[m]) ** 2).sum(-1)            # exact distances of the returned rows
+        tq = TOL * (q64[m] ** 2).sum()
+        dist = od[0, m]
+        assert np.all(d_ret <= dist[k - 1] + tq), (m, "a returned row is not among the nearest")
+        must = oi[0, m, :k][dist[:k] < dist[k] - tq]
+        assert set(must.tolist()) <= set(S.tolist()), (m, "recall")
+        assert np.all(d_ret[:-1] <= d_ret[1:] + tq), (m, "order")
+        err = np.abs(gd_s[m] - d_ret)
+        assert np.all(err <= TOL * ((q64[m] ** 2).sum() + (r64[S] ** 2).sum(-1))), (m, err.max())
