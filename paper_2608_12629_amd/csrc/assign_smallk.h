@@ -56,21 +56,27 @@ __device__ __forceinline__ uint4 onehot8(const int (&iv)[8], int cl) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// The four 32-centroid tiles of one resident stage, in index order.
-template <int DT, int CPL, int LOADS>
+// The first NT (2 or 4) 32-centroid tiles of one resident stage, in index
+// order: K <= 64 needs only two (the rest of the stage is padding).
+template <int DT, int CPL, int LOADS, int NT>
 __device__ __forceinline__ void sk_stage(const uint4 (&xr)[1][CPL], char* buf,
                                          const PipeOffsets<CPL, LOADS>& o, uint32_t tb,
                                          const float (&Qp)[1], float (&best)[1],
                                          uint32_t (&code)[1]) {
+  static_assert(NT == 2 || NT == 4, "two or four tiles");
   f32x16 a0[1], a1[1];
   pipe_mfma_tile<DT, 0, CPL, 1, LOADS>(a0, xr, buf, o);
   pipe_mfma_tile<DT, 1, CPL, 1, LOADS>(a1, xr, buf, o);
   pipe_epilogue<1, true>(a0, tb << 4, best, code, Qp);
-  pipe_mfma_tile<DT, 2, CPL, 1, LOADS>(a0, xr, buf, o);
-  pipe_epilogue<1, true>(a1, (tb + 1) << 4, best, code, Qp);
-  pipe_mfma_tile<DT, 3, CPL, 1, LOADS>(a1, xr, buf, o);
-  pipe_epilogue<1, true>(a0, (tb + 2) << 4, best, code, Qp);
-  pipe_epilogue<1, true>(a1, (tb + 3) << 4, best, code, Qp);
+  if constexpr (NT == 4) {
+    pipe_mfma_tile<DT, 2, CPL, 1, LOADS>(a0, xr, buf, o);
+    pipe_epilogue<1, true>(a1, (tb + 1) << 4, best, code, Qp);
+    pipe_mfma_tile<DT, 3, CPL, 1, LOADS>(a1, xr, buf, o);
+    pipe_epilogue<1, true>(a0, (tb + 2) << 4, best, code, Qp);
+    pipe_epilogue<1, true>(a1, (tb + 3) << 4, best, code, Qp);
+  } else {
+    pipe_epilogue<1, true>(a1, (tb + 1) << 4, best, code, Qp);
+  }
 }
 
 // The LDS area a wave transposes through is its own, so between its writes
@@ -213,7 +219,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_smallk_kernel(
   double obj = 0.0;
   // tile t from xr / ir, with tile t + 2 started into xn / in_; false past the last tile
   auto step = [&](int t, const uint4 (&xr)[1][CPL], int ir, uint4 (&xn)[1][CPL], int& in_) {
-    if (t >= SK_TILES || blockIdx.x * SMALLK_CH + t * SK_TILE >= N) return false;  // uniform
+    if (t >= SK_TILES || (int)blockIdx.x * SMALLK_CH + t * SK_TILE >= N) return false;  // uniform
     const int pt = p0 + t * SK_TILE;
     const bool ok = pt < N;
     // past the last tile, the last tile again (an L2 hit; a branch here would make waits full)
@@ -228,9 +234,9 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_smallk_kernel(
       const float Qp[1] = {__builtin_fmaf(0.5f * ss, 1.0f + 0x1p-8f, 1e-30f)};
       float best[1] = {-__builtin_inff()};
       uint32_t code[1] = {0};
-      sk_stage<DT, CPL, LOADS>(xr, buf0, o, 0, Qp, best, code);
+      sk_stage<DT, CPL, LOADS, KTM < 4 ? 2 : 4>(xr, buf0, o, 0, Qp, best, code);
       if constexpr (TWO)
-        if (Kp > L::TCS) sk_stage<DT, CPL, LOADS>(xr, buf1, o, 4, Qp, best, code);
+        if (Kp > L::TCS) sk_stage<DT, CPL, LOADS, 4>(xr, buf1, o, 4, Qp, best, code);
       float v = best[0];
       const uint32_t j = code[0] & 15u;
       i = (int)((code[0] >> 4) * 32 + 8 * (j >> 2) + 4 * h + (j & 3));

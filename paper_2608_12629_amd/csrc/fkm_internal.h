@@ -20,9 +20,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ---- tuning constants -------------------------------------------------------
-// Assignment (resident-X kernel): 256 threads = 4 waves per workgroup; each
-// wave keeps ASSIGN_NSUB x 16 points in registers; centroids stream through
-// LDS in stages of ASSIGN_TCS rows.
+// Assignment (resident-point kernels): 256 threads = 4 waves per workgroup;
+// each wave keeps NSUB column tiles of points in registers; the fp32 kernel
+// streams its centroids through LDS in stages of ASSIGN_TCS rows.
 constexpr int ASSIGN_THREADS = 256;
 constexpr int ASSIGN_TCS = 64;
 // The rounded centroids and their norms are stored padded to a whole number of
