@@ -116,12 +116,23 @@ __device__ __forceinline__ float knn_pick(const f32x16& acc, int j) {
   return s;
 }
 
-// The top-k update of one tile: the scores that beat the lane's KMAX-th best
-// are marked, and while any lane has a mark left, each lane inserts its
-// lowest marked score (so rows still enter in index order).
+// The top-k update of one tile: unless no lane's best score of the tile beats
+// its KMAX-th best, the scores that do are marked, and while any lane has a
+// mark left, each lane inserts its lowest marked score (so rows still enter
+// in index order).
 template <int KMAX>
 __device__ __forceinline__ void knn_update(const f32x16& acc, int base, float (&v)[KMAX],
                                            int (&ix)[KMAX]) {
+  // first the tile's best score (a max3 tree): once the lists have filled, no
+  // lane's usually beats its KMAX-th best, and the tile costs 8 instructions
+  const float t0 = __builtin_fmaxf(__builtin_fmaxf(acc[0], acc[1]), acc[2]);
+  const float t1 = __builtin_fmaxf(__builtin_fmaxf(acc[3], acc[4]), acc[5]);
+  const float t2 = __builtin_fmaxf(__builtin_fmaxf(acc[6], acc[7]), acc[8]);
+  const float t3 = __builtin_fmaxf(__builtin_fmaxf(acc[9], acc[10]), acc[11]);
+  const float t4 = __builtin_fmaxf(__builtin_fmaxf(acc[12], acc[13]), acc[14]);
+  const float mx = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(t0, t1), t2),
+                                   __builtin_fmaxf(__builtin_fmaxf(t3, t4), acc[15]));
+  if (!__ballot(mx > v[KMAX - 1])) return;
   uint32_t mark = 0;
 #pragma unroll
   for (int j = 0; j < 16; ++j) mark |= (acc[j] > v[KMAX - 1] ? 1u : 0u) << j;
