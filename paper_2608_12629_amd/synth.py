@@ -55,6 +55,11 @@ WORKLOADS = {
     5: dict(name="subspace_n2097152_d1024_k16384_bf16", B=1, N=2_097_152, D=1024, K=16_384,
             dtype="bf16", iters=5, kind="subspace", rank=32, noise=0.05, init="sample",
             seed=0x2608_0005),
+    # the shape the paper times its assignment kernels on (Section 5: B = 32,
+    # N = 65,536, K = 1,024, D = 128, bf16), as 32 independent instances
+    6: dict(name="paper_b32_n65536_d128_k1024_bf16", B=32, N=65_536, D=128, K=1024,
+            dtype="bf16", iters=10, kind="blobs", n_blobs=1024, box=1.0, sigma=0.2,
+            weights="equal", init="sample", seed=0x2608_0006),
 }
 
 _CHUNK_ROWS = 1 << 16
@@ -152,7 +157,7 @@ def _make_instance(spec: dict, N: int, D: int, K: int, seed_seq: np.random.SeedS
 def make_workload(cfg: int, *, N: Optional[int] = None, K: Optional[int] = None,
                   B: Optional[int] = None, D: Optional[int] = None,
                   n_blobs: Optional[int] = None, seed: Optional[int] = None) -> Workload:
-    """Build workload ``cfg`` (1..5), optionally with smaller sizes.
+    """Build workload ``cfg`` (1..6), optionally with smaller sizes.
 
     Overrides keep the recipe and change only the sizes; ``K`` also sets the
     number of blobs unless ``n_blobs`` is given.  The returned tensors live on
