@@ -406,7 +406,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     const int32_t* __restrict__ counts, const int32_t* __restrict__ off,
     const float* C_prev, int K, int D, int nred, int cr, float* C_out, NextStep nx) {
   __shared__ float4 part[256];
-  __shared__ __attribute__((aligned(16))) float row[MAX_D];
+  extern __shared__ float4 row4_dyn[];  // the new centroid row (D floats, sized at launch)
+  float* row = reinterpret_cast<float*>(row4_dyn);
   __shared__ double red[256];
   const int k = blockIdx.x, b = blockIdx.y;
   const int t = threadIdx.x;
@@ -600,7 +601,8 @@ __global__ __launch_bounds__(256) void smallk_combine_kernel(
     int K, int D, int nch, float* C_out, int32_t* __restrict__ counts, NextStep nx) {
   __shared__ int wsum[4];
   __shared__ float4 part[256];
-  __shared__ __attribute__((aligned(16))) float row[MAX_D];
+  extern __shared__ float4 row4_dyn[];  // the new centroid row (D floats, sized at launch)
+  float* row = reinterpret_cast<float*>(row4_dyn);
   __shared__ double red[256];
   const int k = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   int n = 0;
@@ -758,7 +760,7 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
 hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
                           int64_t K, int64_t D, float* C_out, int32_t* counts,
                           const NextStep& nx, hipStream_t s) {
-  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
+  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, D * sizeof(float), s>>>(
       w.partial, w.pcount, C_prev, (int)K, (int)D, (int)nch, C_out, counts, nx);
   return hipGetLastError();
 }
@@ -811,7 +813,7 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
   else if (dt == DT_F16) e = launch_segreduce_dt<DT_F16>(X, w, B, N, D, K, s);
   else e = launch_segreduce_dt<DT_F32>(X, w, B, N, D, K, s);
   if (e != hipSuccess) return e;
-  finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, 0, s>>>(
+  finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, D * sizeof(float), s>>>(
       w.sums, w.carry, counts, w.off, C_prev, (int)K, (int)D, (int)w.n_red_chunks, (int)w.red_cr,
       C_out, nx);
   return hipGetLastError();
