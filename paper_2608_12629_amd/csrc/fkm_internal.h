@@ -117,7 +117,7 @@ inline int64_t kernel_dim(int dt, int64_t D) {
 }
 // Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
 // workgroup; its centroids are padded to whole blocks.
-constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 4;
+constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 8;
 constexpr int64_t TILED_ZERO_BYTES = 16384;  // zeros after the keys (padding stages)
 inline int64_t kpad_for(int dt, int64_t D, int64_t K) {
   return assign_tiled(dt, D) ? (K + TILED_BC - 1) / TILED_BC * TILED_BC : kpad(K);
