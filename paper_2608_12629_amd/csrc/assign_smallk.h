@@ -1,4 +1,4 @@
-// assign_smallk.h -- the Lloyd step for small K (16-bit rows of 32 to 128
+// assign_smallk.h -- the Lloyd step for small K (16-bit rows of 32 to 96
 // elements, K <= 256) in one pass over X: each workgroup assigns 2,048
 // consecutive points and sums them per cluster, so the update's partial sums
 // cost no second read of the points.  The same kernel without the sums is the
@@ -137,7 +137,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_smallk_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
     int N, int K, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
     double* __restrict__ objpart, float* __restrict__ partial, int32_t* __restrict__ pcount) {
-  static_assert(DT != DT_F32 && CPL >= 2 && CPL <= 8, "16-bit rows of 32 to 128 elements");
+  static_assert(DT != DT_F32 && CPL >= 2 && CPL <= 6, "16-bit rows of 32 to 96 elements");
   using L = PipeLayout<CPL>;
   using SL = SkLayout<CPL>;
   constexpr int RC = L::RC, D = 16 * CPL, DTL = SL::DTL;
@@ -363,8 +363,6 @@ hipError_t launch_sums_dt(const void* X, const Workspace& w, int64_t B, int64_t 
     case 4: return launch_smallk_c<DT, 4>(X, w, B, N, K, mode, idx, min_dist, s);
     case 5: return launch_smallk_c<DT, 5>(X, w, B, N, K, mode, idx, min_dist, s);
     case 6: return launch_smallk_c<DT, 6>(X, w, B, N, K, mode, idx, min_dist, s);
-    case 7: return launch_smallk_c<DT, 7>(X, w, B, N, K, mode, idx, min_dist, s);
-    case 8: return launch_smallk_c<DT, 8>(X, w, B, N, K, mode, idx, min_dist, s);
     default: return hipErrorInvalidValue;
   }
 }

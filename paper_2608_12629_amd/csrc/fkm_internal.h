@@ -60,16 +60,18 @@ inline bool smallk_ok(int dt, int64_t D, int64_t K) {
   return K <= (dt == DT_F32 ? 512 : 256) && K * D <= SMALLK_MAX_KD;
 }
 // Small-K kernels with one-hot MFMA sums (the assignment, the update's sums
-// and the fused Lloyd step for these shapes): 16-bit rows of 32 to 128
+// and the fused Lloyd step for these shapes): 16-bit rows of 32 to 96
 // elements and at most 8 per-wave 32x32 sum tiles (128 registers): the
-// ceil(K/32) cluster tiles rounded up to 2, 4 or 8, times ceil(D/32).  The
-// fused step holds the sums beside the assignment's registers: at most 4.
+// ceil(K/32) cluster tiles rounded up to 2, 4 or 8, times ceil(D/32).  (Rows
+// of 112 or 128 elements with their 8 tiles spill beside the three prefetched
+// point tiles.)  The fused step holds the sums beside the assignment's
+// registers: at most 4.
 inline int64_t sums_tiles(int64_t D, int64_t K) {
   const int64_t kt = (K + 31) / 32;
   return (kt <= 2 ? 2 : (kt <= 4 ? 4 : 8)) * ((D + 31) / 32);
 }
 inline bool sums_ok(int dt, int64_t D, int64_t K) {
-  return dt != DT_F32 && D % 16 == 0 && D >= 32 && D <= 128 && K <= 256 && sums_tiles(D, K) <= 8;
+  return dt != DT_F32 && D % 16 == 0 && D >= 32 && D <= 96 && K <= 256 && sums_tiles(D, K) <= 8;
 }
 inline bool fused_ok(int dt, int64_t D, int64_t K) { return sums_ok(dt, D, K) && sums_tiles(D, K) <= 4; }
 // KNN search: k nearest database rows per query, k <= KNN_MAX_K.
