@@ -69,6 +69,12 @@ def test_workspace_bytes(lib):
             cur = ws(1, N, 128, K)
             assert cur >= prev
             prev = cur
+    # the small-K one-hot path (16-bit, D = 64, K = 64)
+    prev = 0
+    for N in (1, 100, 2048, 2049, 4096, 65536, 1 << 20):
+        cur = ws(2, N, 64, 64, F16)
+        assert cur >= prev
+        prev = cur
     # fp32 workgroups shrink for small problems (more of them): still monotone
     for D, K in ((64, 256), (128, 4096)):
         prev = 0
