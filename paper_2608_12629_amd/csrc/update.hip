@@ -375,92 +375,128 @@ __global__ __launch_bounds__(256) void segreduce_kernel(
 // iteration's rounded row and score (wave 0, prep_row: the bits prep would
 // write), and the workgroup of cluster 0 sums the instance's objective
 // partials in fp64 in a fixed order.
-__device__ inline void next_step_tail(const NextStep& nx, const float* row, int64_t b, int k, int D,
-                                      int tid, double* red) {
-  if (nx.chat && tid < 64) {
+__device__ inline void next_step_tail(const NextStep& nx, const float* row, int64_t b, int k,
+                                      bool has_row, int D, int tt, int t, bool obj_block,
+                                      double* red) {
+  if (nx.chat && has_row && tt < 64) {  // the first wave of the cluster's thread group
     const int64_t r = b * nx.Kp + k;
     void* out = (char*)nx.chat + r * D * dt_bytes(nx.dt);
-    if (nx.dt == DT_BF16) prep_row<DT_BF16>(row, false, D, tid, out, nx.cinit + r);
-    else if (nx.dt == DT_F16) prep_row<DT_F16>(row, false, D, tid, out, nx.cinit + r);
-    else prep_row<DT_F32>(row, false, D, tid, out, nx.cinit + r);
+    if (nx.dt == DT_BF16) prep_row<DT_BF16>(row, false, D, tt, out, nx.cinit + r);
+    else if (nx.dt == DT_F16) prep_row<DT_F16>(row, false, D, tt, out, nx.cinit + r);
+    else prep_row<DT_F32>(row, false, D, tt, out, nx.cinit + r);
   }
-  if (nx.objective && k == 0) {
+  if (nx.objective && obj_block) {
+    // a thread adds its partials (every 256th) in index order; the loads go
+    // out OBJ_BATCH at a time (there can be tens of thousands of partials,
+    // and the kernel lasts as long as this workgroup), the adds stay in order
+    constexpr int OBJ_BATCH = 16;
     const double* pb = nx.objpart + b * nx.nparts;
+    const int64_t last = nx.nparts - 1;
     double a = 0.0;
-    for (int64_t i = tid; i < nx.nparts; i += 256) a += pb[i];
-    red[tid] = a;
+    for (int64_t i0 = t; i0 <= last; i0 += 256 * OBJ_BATCH) {
+      double v[OBJ_BATCH];
+#pragma unroll
+      for (int u = 0; u < OBJ_BATCH; ++u) v[u] = pb[min(i0 + 256 * u, last)];
+#pragma unroll
+      for (int u = 0; u < OBJ_BATCH; ++u)
+        if (i0 + 256 * u <= last) a += v[u];
+    }
+    red[t] = a;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {
-      if (tid < w) red[tid] += red[tid + w];
+      if (t < w) red[t] += red[t + w];
       __syncthreads();
     }
-    if (tid == 0) nx.objective[b * nx.iters + nx.t] = red[0];
+    if (t == 0) nx.objective[b * nx.iters + nx.t] = red[0];
   }
 }
 
-// One workgroup per cluster: each thread owns 4 consecutive dimensions; the
-// (256 / (D/4)) row slots split a long list of partials and are combined in
-// a fixed order through LDS.
+// The last update kernels give each cluster a group of threads: one wave for
+// rows of up to 256 floats (four clusters per workgroup), else the whole
+// workgroup.  Within a group each thread owns 4 consecutive dimensions and the
+// group's (threads / (D/4)) row slots each add every slots-th partial in order
+// (loads issued SUM_BATCH at a time, adds in that order); the slot sums are
+// combined in slot order through LDS.  The group size depends on D only.
+constexpr int SUM_BATCH = 8;
+__host__ __device__ inline int final_threads(int D) { return D <= 256 ? 64 : 256; }
+
+__device__ inline float4 f4add(float4 s, float4 v) {
+  return make_float4(s.x + v.x, s.y + v.y, s.z + v.z, s.w + v.w);
+}
+__device__ inline float4 f4div(float4 s, float n) {
+  return make_float4(s.x / n, s.y / n, s.z / n, s.w / n);
+}
+
+// Per cluster, the sum (one slice, or the slices' carries in slice order)
+// over the count; an empty cluster keeps its previous centroid.
 __global__ __launch_bounds__(256) void finalize_kernel(
     const float* __restrict__ sums, const float* __restrict__ carry,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ off,
     const float* C_prev, int K, int D, int nred, int cr, float* C_out, NextStep nx) {
   __shared__ float4 part[256];
-  extern __shared__ float4 row4_dyn[];  // the new centroid row (D floats, sized at launch)
-  float* row = reinterpret_cast<float*>(row4_dyn);
+  extern __shared__ float4 row4_dyn[];  // the groups' new centroid rows (D floats each)
   __shared__ double red[256];
-  const int k = blockIdx.x, b = blockIdx.y;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, b = blockIdx.y;
   const int D4 = D / 4;
-  const int slots = D4 >= 256 ? 1 : 256 / D4;
+  const int TPC = final_threads(D), G = 256 / TPC;
+  const int g = t / TPC, tt = t % TPC;
+  const int k = blockIdx.x * G + g;
+  const bool valid = k < K;
+  float4* row4 = row4_dyn + g * D4;
   const size_t rowoff = ((size_t)b * K + k) * D;
-  float4* row4 = reinterpret_cast<float4*>(row);
-  const int n = counts[(size_t)b * K + k];
-  const int j0 = off[(size_t)b * (K + 1) + k], j1 = off[(size_t)b * (K + 1) + k + 1];
-  const int c0 = j0 / cr, c1 = n == 0 ? c0 : (j1 - 1) / cr;
+  int n = 0, j0 = 0, c0 = 0, c1 = 0;
+  if (valid) {
+    n = counts[(size_t)b * K + k];
+    j0 = off[(size_t)b * (K + 1) + k];
+    const int j1 = off[(size_t)b * (K + 1) + k + 1];
+    c0 = j0 / cr;
+    c1 = n == 0 ? c0 : (j1 - 1) / cr;
+  }
+  const bool multi = valid && n > 0 && c0 != c1;
   const float fn = (float)n;
-  if (n == 0) {
-    for (int d = t; d < D4; d += 256) {
-      const float4 v = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
-      reinterpret_cast<float4*>(C_out + rowoff)[d] = v;
-      row4[d] = v;
-    }
-  } else if (c0 == c1) {
-    for (int d = t; d < D4; d += 256) {
-      const float4 s = reinterpret_cast<const float4*>(sums + rowoff)[d];
-      const float4 m = make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
-      reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
-      row4[d] = m;
-    }
-  } else {
-    const int slot = (D4 >= 256) ? 0 : t / D4;
-    for (int d0 = 0; d0 < D4; d0 += 256) {
-      const int d = d0 + (D4 >= 256 ? t : t % D4);
-      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (slot < slots && d < D4) {
-        for (int c = c0 + slot; c <= c1; c += slots) {
+  const int slots = D4 >= TPC ? 1 : TPC / D4;
+  const int slot = D4 >= TPC ? 0 : tt / D4;
+  for (int d0 = 0; d0 < D4; d0 += TPC) {
+    const int d = d0 + (D4 >= TPC ? tt : tt % D4);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (multi && slot < slots && d < D4) {
+      // slice c holds the cluster's head run in entry 1 when the run starts
+      // inside it (only possible for c0), else in entry 0
+      for (int cb = c0 + slot; cb <= c1; cb += SUM_BATCH * slots) {
+        float4 v[SUM_BATCH];
+#pragma unroll
+        for (int u = 0; u < SUM_BATCH; ++u) {
+          const int c = min(cb + u * slots, c1);
           const int which = (c == c0 && j0 > c * cr) ? 1 : 0;
-          const float4 v = reinterpret_cast<const float4*>(
-              carry + (((size_t)b * nred + c) * 2 + which) * D)[d];
-          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+          v[u] = reinterpret_cast<const float4*>(carry + (((size_t)b * nred + c) * 2 + which) * D)[d];
         }
+#pragma unroll
+        for (int u = 0; u < SUM_BATCH; ++u)
+          if (cb + u * slots <= c1) s = f4add(s, v[u]);
       }
+    }
+    if (slots > 1) {
       __syncthreads();
       part[t] = s;
       __syncthreads();
-      if (slot == 0 && d < D4) {
-        for (int u = 1; u < slots; ++u) {
-          const float4 v = part[u * D4 + (t % D4)];
-          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
-        const float4 m = make_float4(s.x / fn, s.y / fn, s.z / fn, s.w / fn);
-        reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
-        row4[d] = m;
+    }
+    if (valid && slot == 0 && d < D4) {
+      float4 m;
+      if (n == 0) {
+        m = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+      } else if (!multi) {
+        m = f4div(reinterpret_cast<const float4*>(sums + rowoff)[d], fn);
+      } else {
+        for (int u = 1; u < slots; ++u) s = f4add(s, part[g * TPC + u * D4 + tt % D4]);
+        m = f4div(s, fn);
       }
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
+      row4[d] = m;
     }
   }
   __syncthreads();
-  next_step_tail(nx, row, b, k, D, t, red);
+  next_step_tail(nx, reinterpret_cast<const float*>(row4), b, k, valid, D, tt, t,
+                 blockIdx.x == 0, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -591,65 +627,73 @@ __global__ __launch_bounds__(1024) void smallk_partials_kernel(
   }
 }
 
-// One workgroup per cluster: the count (integer sum over chunks), then the
-// partials: each thread owns 4 consecutive dimensions, and the 256 / (D/4)
-// row slots each add every slots-th chunk in chunk order; the slot sums are
-// combined in slot order through LDS and divided by the count.  An empty
-// cluster keeps its previous centroid.
+// Per cluster (thread groups as in finalize_kernel): the count (integer sum
+// over chunks), then the chunk partials added in chunk order and divided by
+// the count.  An empty cluster keeps its previous centroid.
 __global__ __launch_bounds__(256) void smallk_combine_kernel(
     const float* __restrict__ partial, const int32_t* __restrict__ pcount, const float* C_prev,
     int K, int D, int nch, float* C_out, int32_t* __restrict__ counts, NextStep nx) {
-  __shared__ int wsum[4];
+  __shared__ int gcount[4];
   __shared__ float4 part[256];
-  extern __shared__ float4 row4_dyn[];  // the new centroid row (D floats, sized at launch)
-  float* row = reinterpret_cast<float*>(row4_dyn);
+  extern __shared__ float4 row4_dyn[];  // the groups' new centroid rows (D floats each)
   __shared__ double red[256];
-  const int k = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
-  int n = 0;
-  for (int c = t; c < nch; c += 256) n += pcount[((size_t)b * nch + c) * K + k];
-  int total;
-  block_scan256(n, wsum, total);
-  if (t == 0) counts[(size_t)b * K + k] = total;
+  const int t = threadIdx.x, b = blockIdx.y;
   const int D4 = D / 4;
+  const int TPC = final_threads(D), G = 256 / TPC;
+  const int g = t / TPC, tt = t % TPC;
+  const int k = blockIdx.x * G + g;
+  const bool valid = k < K;
+  float4* row4 = row4_dyn + g * D4;
   const size_t rowoff = ((size_t)b * K + k) * D;
-  float4* row4 = reinterpret_cast<float4*>(row);
-  if (total == 0) {
-    for (int d = t; d < D4; d += 256) {
-      const float4 v = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
-      reinterpret_cast<float4*>(C_out + rowoff)[d] = v;
-      row4[d] = v;
+  if (tt < 64) {  // the group's first wave counts
+    int n = 0;
+    if (valid)
+      for (int c = tt; c < nch; c += 64) n += pcount[((size_t)b * nch + c) * K + k];
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) n += __shfl_xor(n, m);
+    if (tt == 0) gcount[g] = n;
+  }
+  __syncthreads();
+  const int total = gcount[g];
+  if (valid && tt == 0) counts[(size_t)b * K + k] = total;
+  const float fn = (float)total;
+  const int slots = D4 >= TPC ? 1 : TPC / D4;
+  const int slot = D4 >= TPC ? 0 : tt / D4;
+  const float4* pb = reinterpret_cast<const float4*>(partial + ((size_t)b * nch * K + k) * D);
+  const size_t cstride = (size_t)K * D4;  // float4s from one chunk's row k to the next chunk's
+  for (int d0 = 0; d0 < D4; d0 += TPC) {
+    const int d = d0 + (D4 >= TPC ? tt : tt % D4);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (valid && total > 0 && slot < slots && d < D4) {
+      for (int cb = slot; cb < nch; cb += SUM_BATCH * slots) {
+        float4 v[SUM_BATCH];
+#pragma unroll
+        for (int u = 0; u < SUM_BATCH; ++u) v[u] = pb[min(cb + u * slots, nch - 1) * cstride + d];
+#pragma unroll
+        for (int u = 0; u < SUM_BATCH; ++u)
+          if (cb + u * slots < nch) s = f4add(s, v[u]);
+      }
     }
-  } else {
-    const float fn = (float)total;
-    const int slots = D4 >= 256 ? 1 : 256 / D4;
-    const int slot = D4 >= 256 ? 0 : t / D4;
-    const float4* pb = reinterpret_cast<const float4*>(partial + ((size_t)b * nch * K + k) * D);
-    const size_t cstride = (size_t)K * D4;  // float4s from one chunk's row k to the next chunk's
-    for (int d0 = 0; d0 < D4; d0 += 256) {
-      const int d = d0 + (D4 >= 256 ? t : t % D4);
-      float4 sacc = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (slot < slots && d < D4) {
-        for (int c = slot; c < nch; c += slots) {
-          const float4 v = pb[c * cstride + d];
-          sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
-        }
-      }
+    if (slots > 1) {
       __syncthreads();
-      part[t] = sacc;
+      part[t] = s;
       __syncthreads();
-      if (slot == 0 && d < D4) {
-        for (int u = 1; u < slots; ++u) {
-          const float4 v = part[u * D4 + (t % D4)];
-          sacc.x += v.x; sacc.y += v.y; sacc.z += v.z; sacc.w += v.w;
-        }
-        const float4 m = make_float4(sacc.x / fn, sacc.y / fn, sacc.z / fn, sacc.w / fn);
-        reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
-        row4[d] = m;
+    }
+    if (valid && slot == 0 && d < D4) {
+      float4 m;
+      if (total == 0) {
+        m = reinterpret_cast<const float4*>(C_prev + rowoff)[d];
+      } else {
+        for (int u = 1; u < slots; ++u) s = f4add(s, part[g * TPC + u * D4 + tt % D4]);
+        m = f4div(s, fn);
       }
+      reinterpret_cast<float4*>(C_out + rowoff)[d] = m;
+      row4[d] = m;
     }
   }
   __syncthreads();
-  next_step_tail(nx, row, b, k, D, t, red);
+  next_step_tail(nx, reinterpret_cast<const float*>(row4), b, k, valid, D, tt, t,
+                 blockIdx.x == 0, red);
 }
 
 template <int DT, int LPR, int CPLR>
@@ -760,7 +804,9 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
 hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
                           int64_t K, int64_t D, float* C_out, int32_t* counts,
                           const NextStep& nx, hipStream_t s) {
-  smallk_combine_kernel<<<dim3((unsigned)K, (unsigned)B), 256, D * sizeof(float), s>>>(
+  const int64_t G = 256 / final_threads((int)D);
+  smallk_combine_kernel<<<dim3((unsigned)((K + G - 1) / G), (unsigned)B), 256,
+                          G * D * sizeof(float), s>>>(
       w.partial, w.pcount, C_prev, (int)K, (int)D, (int)nch, C_out, counts, nx);
   return hipGetLastError();
 }
@@ -813,7 +859,8 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
   else if (dt == DT_F16) e = launch_segreduce_dt<DT_F16>(X, w, B, N, D, K, s);
   else e = launch_segreduce_dt<DT_F32>(X, w, B, N, D, K, s);
   if (e != hipSuccess) return e;
-  finalize_kernel<<<dim3((unsigned)K, (unsigned)B), 256, D * sizeof(float), s>>>(
+  const int64_t G = 256 / final_threads((int)D);
+  finalize_kernel<<<dim3((unsigned)((K + G - 1) / G), (unsigned)B), 256, G * D * sizeof(float), s>>>(
       w.sums, w.carry, counts, w.off, C_prev, (int)K, (int)D, (int)w.n_red_chunks, (int)w.red_cr,
       C_out, nx);
   return hipGetLastError();
