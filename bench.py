@@ -155,6 +155,8 @@ def main():
                          "paper's B=32 assignment shape (context)")
     ap.add_argument("--cold-samples", type=int, default=5,
                     help="assignments timed one by one after evicting the caches (median reported)")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="time the host-launched Lloyd run instead of its graph replay")
     ap.add_argument("--knn", action="store_true", help="measure the KNN search instead")
     ap.add_argument("--knn-queries", type=int, default=262144)
     ap.add_argument("--knn-rows", type=int, default=1 << 20)
@@ -196,15 +198,40 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # warm-up, then exactly `steps` Lloyd iterations from C0
+    # warm-up, then exactly `steps` Lloyd iterations from C0 (host launches)
+    obj = torch.empty((B, args.steps), dtype=torch.float64, device=dev)
     km.kmeans_lloyd(X, C, args.warmup, idx=idx, min_dist=md, counts=cnt, ws=ws)
     C.copy_(C0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    km.kmeans_lloyd(X, C, args.steps, idx=idx, min_dist=md, counts=cnt, ws=ws)
+    km.kmeans_lloyd(X, C, args.steps, idx=idx, min_dist=md, counts=cnt, objective=obj, ws=ws)
     torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    log(f"{args.steps} Lloyd iterations in {dt * 1e3:.2f} ms")
+    dt = dt_eager = time.perf_counter() - t0
+    log(f"{args.steps} Lloyd iterations in {dt * 1e3:.2f} ms (host launches)")
+    if args.graph:
+        # the same run captured once in a HIP graph: `warmup` untimed replays,
+        # then one timed replay of exactly `steps` iterations, checked bit for
+        # bit against the run above
+        C_ref, obj_ref, idx_ref = C.clone(), obj.clone(), idx.clone()
+        C.copy_(C0)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            km.kmeans_lloyd(X, C, args.steps, idx=idx, min_dist=md, counts=cnt, objective=obj,
+                            ws=ws)
+        for _ in range(args.warmup):
+            C.copy_(C0)
+            graph.replay()
+        C.copy_(C0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        graph.replay()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        log(f"{args.steps} Lloyd iterations in {dt * 1e3:.2f} ms (graph replay)")
+        if not (torch.equal(C, C_ref) and torch.equal(obj, obj_ref) and torch.equal(idx, idx_ref)):
+            raise SystemExit("graph replay differs from the host-launched run")
+        del graph, C_ref, obj_ref, idx_ref
 
     # per-kernel durations with HIP events on the stream the library launches on
     stream = torch.cuda.current_stream()
@@ -266,7 +293,9 @@ def main():
         "dtype": {"bf16": "bf16", "f16": "f16", "f32": "f32"}[w.dtype],
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "N": N, "D": D, "K": K, "x_dtype": w.dtype,
-                   "centroid_dtype": "f32", "iters_per_step": 1},
+                   "centroid_dtype": "f32", "iters_per_step": 1,
+                   "launch": "graph replay" if args.graph else "host"},
+        "host_launch_ms_per_step": dt_eager * 1e3 / args.steps,
         "roofline": roofline,
         "update": {"ms": update_ms, "algorithmic_bytes": upd_bytes, "GB/s": upd_gbs,
                    "hbm_frac": upd_gbs / PEAK_HBM_GBS},

@@ -151,10 +151,13 @@ def kmeans_update(X: torch.Tensor, idx: torch.Tensor, C_prev: torch.Tensor,
 
 def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
                  idx: Optional[torch.Tensor] = None, min_dist: Optional[torch.Tensor] = None,
-                 counts: Optional[torch.Tensor] = None, objective: bool = True,
+                 counts: Optional[torch.Tensor] = None, objective=True,
                  ws: Optional[Workspace] = None):
     """Run ``iters`` Lloyd iterations, updating C in place.
 
+    ``objective``: True (a new [B, iters] fp64 tensor), False (none), or a
+    [B, iters] fp64 device tensor to write into (nothing is allocated when
+    every output and ``ws`` are given, so the call can be captured in a graph).
     Returns (C, idx, min_dist, counts, objective[B, iters] fp64 or None).
     """
     B, N, D, K = _shapes(X, C)
@@ -164,7 +167,13 @@ def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
     idx = torch.empty((B, N), dtype=torch.int32, device=dev) if idx is None else idx
     min_dist = torch.empty((B, N), dtype=torch.float32, device=dev) if min_dist is None else min_dist
     counts = torch.empty((B, K), dtype=torch.int32, device=dev) if counts is None else counts
-    obj = torch.empty((B, iters), dtype=torch.float64, device=dev) if objective else None
+    if isinstance(objective, torch.Tensor):
+        obj = objective
+        _need(obj, "objective", torch.float64)
+        if tuple(obj.shape) != (B, iters):
+            raise ValueError(f"objective has shape {tuple(obj.shape)}, want {(B, iters)}")
+    else:
+        obj = torch.empty((B, iters), dtype=torch.float64, device=dev) if objective else None
     for t, name, dt in ((idx, "idx", torch.int32), (min_dist, "min_dist", torch.float32),
                         (counts, "counts", torch.int32)):
         _need(t, name, dt)
