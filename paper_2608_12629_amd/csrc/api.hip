@@ -41,8 +41,10 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
   w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
   w.objpart = (double*)take((size_t)(B * nparts) * 8);
-  w.rhist = (int32_t*)take((size_t)(B * RADIX_MAX_R * w.n_sort_chunks) * 4);
+  // the second packed pass cuts at most RADIX_MAX_R more chunks (one per low digit)
+  w.rhist = (int32_t*)take((size_t)(B * RADIX_MAX_R * (w.n_sort_chunks + RADIX_MAX_R)) * 4);
   w.rbin = (int32_t*)take((size_t)B * RADIX_MAX_R * 4);
+  w.rbin1 = (int32_t*)take((size_t)B * RADIX_MAX_R * 4);
   w.rtotal = (int32_t*)take((size_t)B * 4);
   w.keys_a = (int32_t*)take((size_t)(B * N) * 4);
   w.vals_a = (int32_t*)take((size_t)(B * N) * 4);

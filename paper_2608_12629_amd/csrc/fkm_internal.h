@@ -130,8 +130,9 @@ struct Workspace {
   void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad_for(dt, D, K))
   float* cinit;    // [B,Kp]   -1/2 * squared norm of each rounded centroid
   double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
-  int32_t* rhist;  // [B,R,n_sort_chunks] radix histograms, then run starts (R <= 256)
+  int32_t* rhist;  // [B,R,chunks] radix histograms, then run starts (R <= 256; chunks <= n_sort_chunks + 256)
   int32_t* rbin;   // [B,256] radix bin totals
+  int32_t* rbin1;  // [B,256] the first pass's bin totals (packed two-pass sort)
   int32_t* rtotal; // [B] number of valid entries (ids in [0, K))
   int32_t* keys_a; // [B,N] cluster ids after the first radix pass
   int32_t* vals_a; // [B,N] point ids after the first radix pass

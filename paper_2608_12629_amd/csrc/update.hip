@@ -6,11 +6,15 @@
 //   1. a stable radix sort of the point ids by cluster id (one or two passes of
 //      histogram, scan and LDS-staged scatter; see below)
 //   2. bounds     per cluster, its run [off_k, off_k+1) in the sorted order
+//                 (after two packed passes: read off the second pass's
+//                 histogram, no sorted keys needed)
 //   3. segreduce  one wave per slice of consecutive sorted entries streams the
 //                 whole rows X[perm[j]] and sums each cluster run in fp32 in a
 //                 fixed order; a run cut by a chunk end leaves a partial
 //   4. finalize   per cluster, the sum (or its partials, in chunk order) over
 //                 the count; an empty cluster keeps its previous centroid.
+#include <algorithm>
+
 #include "fkm_device.h"
 
 namespace fkm {
@@ -59,15 +63,55 @@ __device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
   return block_scan<4>(v, wsum, total);
 }
 
+// The second packed pass cuts each bin of the first pass (the entries with one
+// low digit, contiguous after that pass: bin r holds T1[r] entries from its
+// start) into chunks of at most RADIX_CHUNK entries, ceil(T1[r] / RADIX_CHUNK)
+// of them, numbered bin by bin, so every chunk holds a single low digit.
+// Chunk `ch` of instance b: entries [e0, e1) with low digit `lo` (an empty
+// range past the last chunk).  Called by all 256 threads; wsum: 8 ints.
+__device__ inline void lo_chunk(const int32_t* __restrict__ T1, int b, int R1, int ch, int* wsum,
+                                int* sel, int& e0, int& e1, int& lo) {
+  const int t = threadIdx.x;
+  const int cnt = t < R1 ? T1[(size_t)b * RADIX_MAX_R + t] : 0;
+  const int q = (cnt + RADIX_CHUNK - 1) / RADIX_CHUNK;
+  int all;
+  const int start = block_scan256(cnt, wsum, all);
+  const int cq = block_scan256(q, wsum + 4, all);
+  if (t == 0) sel[0] = sel[1] = sel[2] = 0;
+  __syncthreads();
+  if (q > 0 && cq <= ch && ch < cq + q) {  // one thread at most
+    const int a = start + (ch - cq) * RADIX_CHUNK;
+    sel[0] = a;
+    sel[1] = min(a + RADIX_CHUNK, start + cnt);
+    sel[2] = t;
+  }
+  __syncthreads();
+  e0 = sel[0];
+  e1 = sel[1];
+  lo = sel[2];
+}
+
 }  // namespace
 
+// pb > 0: the entries are packed words (digit above pb point-id bits) in the
+// chunks of lo_chunk (T1: the first pass's bin totals).
 __global__ __launch_bounds__(256) void radix_hist_kernel(const int32_t* __restrict__ keys, int N,
                                                          int K, const int32_t* __restrict__ total,
                                                          int shift, int R, int nch,
-                                                         int32_t* __restrict__ H) {
+                                                         int32_t* __restrict__ H, int pb,
+                                                         const int32_t* __restrict__ T1,
+                                                         int lo_bits) {
   __shared__ int cnt[RADIX_MAX_R];
+  __shared__ int wsum[8], sel[3];
   const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
-  const int n_in = total ? total[b] : N;  // later passes read the valid prefix only
+  int e0, e1, lo;
+  if (pb) {
+    lo_chunk(T1, b, 1 << lo_bits, ch, wsum, sel, e0, e1, lo);
+  } else {
+    const int n_in = total ? total[b] : N;  // later passes read the valid prefix only
+    e0 = ch * RADIX_CHUNK;
+    e1 = min(e0 + RADIX_CHUNK, n_in);
+  }
   for (int r = t; r < R; r += 256) cnt[r] = 0;
   __syncthreads();
   const int32_t* kb = keys + (size_t)b * N;
@@ -75,12 +119,17 @@ __global__ __launch_bounds__(256) void radix_hist_kernel(const int32_t* __restri
   int k[PER];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    const int i = ch * RADIX_CHUNK + u * 256 + t;
-    k[u] = i < n_in ? kb[i] : -1;
+    const int i = e0 + u * 256 + t;
+    k[u] = i < e1 ? kb[i] : -1;
   }
 #pragma unroll
-  for (int u = 0; u < PER; ++u)
-    if ((unsigned)k[u] < (unsigned)K) atomicAdd(&cnt[digit_of(k[u], shift, R)], 1);
+  for (int u = 0; u < PER; ++u) {
+    if (pb) {
+      if (k[u] >= 0) atomicAdd(&cnt[(k[u] >> pb) & (R - 1)], 1);
+    } else if ((unsigned)k[u] < (unsigned)K) {
+      atomicAdd(&cnt[digit_of(k[u], shift, R)], 1);
+    }
+  }
   __syncthreads();
   for (int r = t; r < R; r += 256) H[((size_t)b * R + r) * nch + ch] = cnt[r];
 }
@@ -117,30 +166,43 @@ __global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H
   if (t == 0) T[(size_t)b * RADIX_MAX_R + r] = bin_total;
 }
 
-template <int DBITS>
+// MODE 0: (key, value) arrays in and out (values default to the entry index).
+// MODE 1 (first of two passes, packed): keys in, one packed word out per entry,
+//   (key >> lo_bits) << pb | point id.
+// MODE 2 (second pass, packed): packed words in, in the chunks of lo_chunk,
+//   so a chunk's low digit is known and restores each key; point ids out.
+template <int DBITS, int MODE>
 __global__ __launch_bounds__(256) void radix_scatter_kernel(
     const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int N, int K,
     const int32_t* __restrict__ total, int shift, int nch,
     const int32_t* __restrict__ H, const int32_t* __restrict__ T, int32_t* __restrict__ total_out,
-    int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
+    int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out, int lo_bits, int pb,
+    const int32_t* __restrict__ T1) {
   constexpr int STEPS = RADIX_CHUNK / 256;  // 64-entry steps per wave
   __shared__ int skey[RADIX_CHUNK], sval[RADIX_CHUNK];
   __shared__ int cur[4][RADIX_MAX_R];
   __shared__ int lstart[RADIX_MAX_R], gstart[RADIX_MAX_R];
-  __shared__ int wsum[2][4];
+  __shared__ int wsum[4][4], sel[3];
   constexpr int R = 1 << DBITS;
   const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
-  const int n_in = total ? total[b] : N;
+  int e0, e1, lo_c = 0;
+  if constexpr (MODE == 2) {
+    lo_chunk(T1, b, 1 << lo_bits, ch, &wsum[2][0], sel, e0, e1, lo_c);
+  } else {
+    const int n_in = total ? total[b] : N;
+    e0 = ch * RADIX_CHUNK;
+    e1 = min(e0 + RADIX_CHUNK, n_in);
+  }
   const int32_t* kb = keys_in + (size_t)b * N;
   const int32_t* vb = vals_in ? vals_in + (size_t)b * N : nullptr;
-  const int ibase = ch * RADIX_CHUNK + w * (RADIX_CHUNK / 4);
+  const int ibase = e0 + w * (RADIX_CHUNK / 4);
 
   int k[STEPS], v[STEPS];
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
     const int i = ibase + s * 64 + lane;
-    const bool in = i < n_in;
+    const bool in = i < e1;
     k[s] = in ? kb[i] : -1;
     v[s] = in ? (vb ? vb[i] : i) : 0;
   }
@@ -153,6 +215,16 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   int n_valid;
   const int bstart = block_scan256(tbin, wsum[0], n_valid);
   if (total_out && ch == 0 && t == 0) total_out[b] = n_valid;
+  if constexpr (MODE == 2) {  // key = high digit (packed) above the chunk's low digit
+    const int pmask = (int)((1u << pb) - 1u);
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (k[s] >= 0) {
+        v[s] = k[s] & pmask;
+        k[s] = ((k[s] >> pb) << lo_bits) | lo_c;
+      }
+    }
+  }
   // per-wave bin counts (integer atomics: exact)
 #pragma unroll
   for (int s = 0; s < STEPS; ++s)
@@ -214,8 +286,50 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
       const int dg = digit_of(key, shift, R);
       const int g = gstart[dg] + (j - lstart[dg]);
       if (ko) ko[g] = key;
-      vo[g] = sval[j];
+      vo[g] = MODE == 1 ? (((key >> lo_bits) << pb) | sval[j]) : sval[j];
     }
+  }
+}
+
+// Cluster offsets and counts after the packed passes (no sorted keys, no
+// atomics): for key k = (hi, lo), off[k] = the entries of lower high digits
+// plus those of digit hi in the chunks before lo's first chunk (the second
+// pass's scanned histogram at that chunk; all of digit hi past the last
+// chunk); count_k = off[k+1] - off[k], off[K] = the valid total.  One key per
+// thread; offsets are capped to [0, total].
+__global__ __launch_bounds__(256) void offsets_kernel(const int32_t* __restrict__ Hs,
+                                                      const int32_t* __restrict__ T2,
+                                                      const int32_t* __restrict__ T1,
+                                                      const int32_t* __restrict__ total, int K,
+                                                      int lo_bits, int R2, int nch2,
+                                                      int32_t* __restrict__ off,
+                                                      int32_t* __restrict__ counts) {
+  __shared__ int wsum[2][4];
+  __shared__ int cq_s[RADIX_MAX_R], bs_s[RADIX_MAX_R], t2_s[RADIX_MAX_R], off_s[256];
+  const int b = blockIdx.y, t = threadIdx.x;
+  const int k = blockIdx.x * 256 + t;  // 0 .. K
+  const int R1 = 1 << lo_bits;
+  const int c1 = t < R1 ? T1[(size_t)b * RADIX_MAX_R + t] : 0;
+  int all;
+  cq_s[t] = block_scan256((c1 + RADIX_CHUNK - 1) / RADIX_CHUNK, wsum[0], all);
+  const int t2 = t < R2 ? T2[(size_t)b * RADIX_MAX_R + t] : 0;
+  t2_s[t] = t2;
+  bs_s[t] = block_scan256(t2, wsum[1], all);
+  __syncthreads();
+  const int nv = total[b];
+  const int32_t* hb = Hs + (size_t)b * R2 * nch2;
+  auto at = [&](int kk) -> int {
+    if (kk >= K) return nv;
+    const int hi = kk >> lo_bits, c = cq_s[kk & (R1 - 1)];
+    const int before = c < nch2 ? hb[(size_t)hi * nch2 + c] : t2_s[hi];
+    return min(max(bs_s[hi] + before, 0), nv);
+  };
+  const int a = k <= K ? at(k) : 0;
+  off_s[t] = a;
+  __syncthreads();
+  if (k <= K) {
+    off[(size_t)b * (K + 1) + k] = a;
+    if (k < K) counts[(size_t)b * K + k] = (t < 255 ? off_s[t + 1] : at(k + 1)) - a;
   }
 }
 
@@ -775,17 +889,17 @@ static hipError_t launch_segreduce_dt(const void* X, const Workspace& w, int64_t
 
 hipError_t update_init() { return hipSuccess; }
 
-template <typename... A>
+template <int MODE, typename... A>
 static hipError_t launch_scatter(int dbits, dim3 grid, hipStream_t s, A... a) {
   switch (dbits) {
-    case 1: radix_scatter_kernel<1><<<grid, 256, 0, s>>>(a...); break;
-    case 2: radix_scatter_kernel<2><<<grid, 256, 0, s>>>(a...); break;
-    case 3: radix_scatter_kernel<3><<<grid, 256, 0, s>>>(a...); break;
-    case 4: radix_scatter_kernel<4><<<grid, 256, 0, s>>>(a...); break;
-    case 5: radix_scatter_kernel<5><<<grid, 256, 0, s>>>(a...); break;
-    case 6: radix_scatter_kernel<6><<<grid, 256, 0, s>>>(a...); break;
-    case 7: radix_scatter_kernel<7><<<grid, 256, 0, s>>>(a...); break;
-    case 8: radix_scatter_kernel<8><<<grid, 256, 0, s>>>(a...); break;
+    case 1: radix_scatter_kernel<1, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 2: radix_scatter_kernel<2, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 3: radix_scatter_kernel<3, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 4: radix_scatter_kernel<4, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 5: radix_scatter_kernel<5, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 6: radix_scatter_kernel<6, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 7: radix_scatter_kernel<7, MODE><<<grid, 256, 0, s>>>(a...); break;
+    case 8: radix_scatter_kernel<8, MODE><<<grid, 256, 0, s>>>(a...); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -799,6 +913,36 @@ static void radix_plan(int64_t K, int& passes, int& d1, int& d2) {
   passes = bits <= RADIX_MAX_BITS ? 1 : 2;
   d1 = passes == 1 ? bits : (bits + 1) / 2;
   d2 = bits - (passes == 1 ? 0 : d1);
+}
+
+// Bits that hold a point id below N (at least 1).
+static int pid_bits(int64_t N) {
+  int p = 1;
+  while ((1ll << p) < N) ++p;
+  return p;
+}
+
+// Digits of the packed passes: the second pass's chunks hold one low digit
+// each, so the low digit gets at most log2(N / RADIX_CHUNK) bits (bins of at
+// least a chunk on average) but at least what leaves the high digit <= 8
+// bits; within that, the split nearest to half.
+static void radix_plan_packed(int64_t N, int64_t K, int& d1, int& d2) {
+  int bits = 1;
+  while ((1ll << bits) < K) ++bits;
+  int fill = 0;
+  while ((RADIX_CHUNK << (fill + 1)) <= N) ++fill;
+  d1 = std::max(bits - RADIX_MAX_BITS, std::min((bits + 1) / 2, fill));
+  d2 = bits - d1;
+}
+
+// Two passes go over one array of packed words when the high digit and the
+// point id fit a non-negative int (31 bits).
+static bool sort_packed(int64_t N, int64_t K) {
+  int passes, d1, d2;
+  radix_plan(K, passes, d1, d2);
+  if (passes != 2) return false;
+  radix_plan_packed(N, K, d1, d2);
+  return d2 + pid_bits(N) <= 31;
 }
 
 hipError_t launch_combine(const Workspace& w, int64_t nch, const float* C_prev, int64_t B,
@@ -824,37 +968,76 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
     return launch_update_smallk(X, dt, idx, C_prev, w, B, N, D, K, C_out, counts, nx, s);
   hipError_t e;
   const int nch = (int)w.n_sort_chunks;
+  const dim3 cgrid(nch, (unsigned)B);
   int passes, d1, d2;
   radix_plan(K, passes, d1, d2);
-  // pass 1: idx (raw) -> (keys_a, vals_a) sorted by the low digit; with one
-  // pass the values go straight to perm and the keys to keys_b
-  {
+  if (sort_packed(N, K)) {
+    radix_plan_packed(N, K, d1, d2);
+    // two passes over one array: pass 1 sorts by the low digit and writes
+    // (high digit, point id) words; pass 2 sorts those by the high digit in
+    // chunks of one low digit each and writes the point ids; the offsets and
+    // counts come from pass 2's histogram
+    const int pb = pid_bits(N);
+    const int R1 = 1 << d1, R2 = 1 << d2;
+    const int nch2 = nch + R1;  // chunks of one low digit: at most this many
+    radix_hist_kernel<<<cgrid, 256, 0, s>>>(idx, (int)N, (int)K, nullptr, 0, R1, nch, w.rhist, 0,
+                                            nullptr, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scan_kernel<<<dim3(R1, (unsigned)B), 256, 0, s>>>(w.rhist, R1, nch, w.rbin1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scatter<1>(d1, cgrid, s, idx, (const int32_t*)nullptr, (int)N, (int)K,
+                               (const int32_t*)nullptr, 0, nch, (const int32_t*)w.rhist,
+                               (const int32_t*)w.rbin1, w.rtotal, (int32_t*)nullptr, w.keys_a, d1,
+                               pb, (const int32_t*)nullptr)) != hipSuccess)
+      return e;
+    const dim3 cgrid2(nch2, (unsigned)B);
+    radix_hist_kernel<<<cgrid2, 256, 0, s>>>(w.keys_a, (int)N, (int)K, nullptr, 0, R2, nch2,
+                                             w.rhist, pb, w.rbin1, d1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    radix_scan_kernel<<<dim3(R2, (unsigned)B), 256, 0, s>>>(w.rhist, R2, nch2, w.rbin);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scatter<2>(d2, cgrid2, s, (const int32_t*)w.keys_a, (const int32_t*)nullptr,
+                               (int)N, (int)K, (const int32_t*)nullptr, d1, nch2,
+                               (const int32_t*)w.rhist, (const int32_t*)w.rbin, (int32_t*)nullptr,
+                               (int32_t*)nullptr, w.perm, d1, pb,
+                               (const int32_t*)w.rbin1)) != hipSuccess)
+      return e;
+    offsets_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
+        w.rhist, w.rbin, w.rbin1, w.rtotal, (int)K, d1, R2, nch2, w.off, counts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
+    // pass 1: idx (raw) -> (keys_a, vals_a) sorted by the low digit; with one
+    // pass the values go straight to perm and the keys to keys_b
     const int R = 1 << d1;
-    radix_hist_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(idx, (int)N, (int)K, nullptr, 0, R, nch,
-                                                            w.rhist);
+    radix_hist_kernel<<<cgrid, 256, 0, s>>>(idx, (int)N, (int)K, nullptr, 0, R, nch, w.rhist, 0,
+                                            nullptr, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = launch_scatter(d1, dim3(nch, (unsigned)B), s, idx, nullptr, (int)N, (int)K, nullptr, 0,
-                            nch, w.rhist, w.rbin, w.rtotal, passes == 1 ? w.keys_b : w.keys_a,
-                            passes == 1 ? w.perm : w.vals_a)) != hipSuccess)
+    if ((e = launch_scatter<0>(d1, cgrid, s, idx, (const int32_t*)nullptr, (int)N, (int)K,
+                               (const int32_t*)nullptr, 0, nch, (const int32_t*)w.rhist,
+                               (const int32_t*)w.rbin, w.rtotal,
+                               passes == 1 ? w.keys_b : w.keys_a, passes == 1 ? w.perm : w.vals_a,
+                               0, 0, (const int32_t*)nullptr)) != hipSuccess)
       return e;
-  }
-  if (passes == 2) {
-    const int R = 1 << d2;
-    radix_hist_kernel<<<dim3(nch, (unsigned)B), 256, 0, s>>>(w.keys_a, (int)N, (int)K, w.rtotal, d1,
-                                                            R, nch, w.rhist);
+    if (passes == 2) {
+      const int R2 = 1 << d2;
+      radix_hist_kernel<<<cgrid, 256, 0, s>>>(w.keys_a, (int)N, (int)K, w.rtotal, d1, R2, nch,
+                                              w.rhist, 0, nullptr, 0);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      radix_scan_kernel<<<dim3(R2, (unsigned)B), 256, 0, s>>>(w.rhist, R2, nch, w.rbin);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if ((e = launch_scatter<0>(d2, cgrid, s, (const int32_t*)w.keys_a, (const int32_t*)w.vals_a,
+                                 (int)N, (int)K, (const int32_t*)w.rtotal, d1, nch,
+                                 (const int32_t*)w.rhist, (const int32_t*)w.rbin, (int32_t*)nullptr,
+                                 w.keys_b, w.perm, 0, 0,
+                                 (const int32_t*)nullptr)) != hipSuccess)  // the same total
+        return e;
+    }
+    bounds_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
+        w.keys_b, w.rtotal, (int)N, (int)K, w.off, counts);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    radix_scan_kernel<<<dim3(R, (unsigned)B), 256, 0, s>>>(w.rhist, R, nch, w.rbin);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = launch_scatter(d2, dim3(nch, (unsigned)B), s, w.keys_a, w.vals_a, (int)N, (int)K,
-                            w.rtotal, d1, nch, w.rhist, w.rbin, nullptr, w.keys_b,
-                            w.perm)) != hipSuccess)  // the second pass keeps the same total
-      return e;
   }
-  bounds_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
-      w.keys_b, w.rtotal, (int)N, (int)K, w.off, counts);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   if (dt == DT_BF16) e = launch_segreduce_dt<DT_BF16>(X, w, B, N, D, K, s);
   else if (dt == DT_F16) e = launch_segreduce_dt<DT_F16>(X, w, B, N, D, K, s);
   else e = launch_segreduce_dt<DT_F32>(X, w, B, N, D, K, s);

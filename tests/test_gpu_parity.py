@@ -107,6 +107,18 @@ def test_full_size_sampled(km, oracle, cfg):
     teacher_forced(km, oracle, w.X, w.C0, w.dtype, 2, rows=rows)
 
 
+def test_unpacked_sort_full(km, oracle):
+    """N = 2^23 + 4,096 points with K = 65,536: the second radix digit (8 bits)
+    and a point id (24 bits) do not fit one int, so the update sorts separate
+    key and value arrays and finds the cluster bounds by binary search (every
+    smaller problem takes the packed passes).  Assignment on sampled rows,
+    update in full."""
+    w = make_workload(3, N=(1 << 23) + 4096, K=65536, D=16)
+    rows = np.sort(np.random.default_rng(7).choice(w.N, 2048, replace=False))
+    say(f"[unpacked sort] {w.name}")
+    teacher_forced(km, oracle, w.X, w.C0, w.dtype, 1, rows=rows)
+
+
 # --------------------------------------------------------------- edge cases
 def _blobs(B, N, D, K, dtype, seed, spread=1.0):
     g = torch.Generator().manual_seed(seed)
@@ -150,6 +162,7 @@ SHAPES = [
     (1, 1500, 384, 300, "bf16"),      # tiled kernel, D = 384
     (1, 1200, 288, 90, "f16"),        # tiled, D = 288: 9 stages + 3 padding stages per block
     (2, 900, 416, 257, "bf16"),       # tiled, D = 416: 13 + 3
+    (4, 20000, 128, 1024, "bf16"),    # batched two-pass sort (packed words), ragged chunks
     (1, 700, 992, 40, "bf16"),        # tiled, D = 992: 31 + 1
     (1, 1000, 512, 130, "bf16"),      # tiled kernel: ragged N and K
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
