@@ -29,6 +29,10 @@
  * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *   the call returns without synchronizing.  Results are deterministic:
  *   identical inputs give bit-identical outputs.
+ * - A call enqueues kernel launches only (no memory set or copy commands, no
+ *   host synchronization, no allocation), so it can be captured into a HIP
+ *   graph and replayed; the first call on a device also reads the device's
+ *   properties once, so make one call before capturing.
  * - `ws` is a device workspace of at least kmeans_workspace_bytes(...) bytes.
  *   Its contents are scratch; calls that share a workspace must be ordered on
  *   one stream.
