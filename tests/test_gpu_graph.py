@@ -1,4 +1,5 @@
-"""GPU: kmeans_lloyd captured in a HIP graph (torch.cuda.CUDAGraph) and replayed.
+"""GPU: kmeans_lloyd and kmeans_knn captured in a HIP graph (torch.cuda.CUDAGraph)
+and replayed.
 
 The library enqueues only kernel launches on the caller's stream (no memsets,
 no host synchronisation, no allocation when the workspace and every output are
@@ -115,3 +116,42 @@ def test_lloyd_graph_replays_equal_eager(km, case):
         assert torch.equal(md_g, md_e), f"replay {r}: min_dist differs"
         assert torch.equal(cnt_g, cnt_e), f"replay {r}: counts differ"
         assert torch.equal(obj_g, obj_e), f"replay {r}: objective differs"
+
+
+@pytest.mark.parametrize("k", [10, 32])
+def test_knn_graph_replays_equal_eager(km, k):
+    """kmeans_knn captured in a graph (workspace and outputs preallocated):
+    every replay, with other eager searches on the same workspace between
+    them, equals the eager result bit for bit."""
+    g = torch.Generator().manual_seed(100 + k)
+    B, M, N, D = 2, 3000, 20000, 128
+    Q = torch.randn((B, M, D), generator=g).to(torch.bfloat16).cuda()
+    R = torch.randn((B, N, D), generator=g).to(torch.bfloat16).cuda()
+    say(f"[graph knn] B={B} M={M} N={N} D={D} k={k}")
+    need = km.knn_workspace_bytes(B, M, N, D, k, torch.bfloat16)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    i_e = torch.empty((B, M, k), dtype=torch.int32, device="cuda")
+    d_e = torch.empty((B, M, k), dtype=torch.float32, device="cuda")
+    km.kmeans_knn(Q, R, k, nbr_idx=i_e, nbr_dist=d_e, ws=ws)
+    torch.cuda.synchronize()
+    i_g, d_g = torch.empty_like(i_e), torch.empty_like(d_e)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        km.kmeans_knn(Q, R, k, nbr_idx=i_g, nbr_dist=d_g, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        km.kmeans_knn(Q, R, k, nbr_idx=i_g, nbr_dist=d_g, ws=ws)
+    torch.cuda.synchronize()
+    for r in range(3):
+        km.kmeans_knn(R[:, :M].contiguous(), Q, k, ws=ws)  # other work on the same workspace
+        i_g.fill_(-1)
+        d_g.fill_(-1.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        say(f"[graph knn]   replay {r}")
+        assert torch.equal(i_g, i_e), f"replay {r}: neighbours differ from the eager run"
+        assert torch.equal(d_g, d_e), f"replay {r}: distances differ"
