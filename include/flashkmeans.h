@@ -93,8 +93,9 @@ int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t 
 /*
  * Centroid update (paper Section 5: reduce the points of each cluster into a
  * per-cluster sum and count).  The reduction is a stable radix sort of the
- * point ids by cluster followed by a segmented sum in fp32 in a fixed order; no
- * floating-point atomics are used.
+ * point ids by cluster followed by a segmented sum in fp32 in a fixed order;
+ * with few clusters (small K * D) it is per-chunk partial sums instead, added
+ * in chunk order.  No floating-point atomics are used.
  *   X       [B, N, D] xdtype  points (read)
  *   idx     [B, N]    int32   cluster of each point (read); a value outside
  *                             [0, K) excludes that point from every count and sum
