@@ -18,7 +18,10 @@
  * - Centroids are fp32: [B, K, D].  The assignment rounds them once to the
  *   storage type (round-to-nearest-even) to feed the matrix cores and uses the
  *   squared norm of the rounded centroid, so each distance is the distance to
- *   that rounded centroid, accumulated in fp32.
+ *   that rounded centroid, accumulated in fp32.  Exception: bf16/fp16 rows of
+ *   at most 16 elements run as fp32 on exactly widened copies of the points
+ *   (made in the workspace), so there the distances are to the fp32
+ *   centroids themselves.
  * - Indices are int32 and local to an instance: idx[b, i] is in [0, K).
  * - Points and centroids must be finite.  (Non-finite values give unspecified
  *   results; with small K the sums are formed by multiplying every point by a
@@ -45,7 +48,8 @@
  *   points and centroids in zero-padded rows of the next such width, made in
  *   the workspace at the start of each call (once per kmeans_lloyd call):
  *   zeros change no distance, sum or norm, so the results are those of the
- *   unpadded rows, at the cost of that copy.
+ *   unpadded rows, at the cost of that copy.  (bf16/fp16 rows of at most 16
+ *   elements are copied into fp32 rows of 16, see above.)
  *   FKM_ERR_HIP reports a failed HIP call or launch.  No C++ exception
  *   crosses this boundary.
  */

@@ -13,11 +13,14 @@ namespace fkm {
 static size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 // The workspace for rows of D elements; every kernel runs at w.Dk (equal to D
-// unless D needs zero-padded copies of the points and centroids).
-Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int dt) {
+// unless D needs zero-padded copies of the points and centroids) in storage
+// type w.kdt (the caller's, unless narrow 16-bit rows run widened to fp32).
+Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int dt_user) {
   Workspace w{};
-  const int64_t D = kernel_dim(dt, D_user);
+  const int64_t D = kernel_dim(dt_user, D_user);
+  const int dt = kernel_dt(dt_user, D_user);
   w.Dk = D;
+  w.kdt = dt;
   if (assign_tiled(dt, D)) {
     w.n_assign_blocks = (N + 255) / 256;  // the decode kernel's blocks
   } else {
@@ -41,6 +44,9 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   w.chat = take((size_t)(B * w.Kp * D) * dt_bytes(dt));
   w.cinit = (float*)take((size_t)(B * w.Kp) * 4);
   w.objpart = (double*)take((size_t)(B * nparts) * 8);
+  // flags of the 16-bit streaming assignment (one per block of points)
+  const bool streaming16 = dt != DT_F32 && !assign_tiled(dt, D);
+  w.wide = (int32_t*)take(streaming16 ? (size_t)(B * w.n_assign_blocks) * 4 : 0);
   // the second packed pass cuts at most RADIX_MAX_R more chunks (one per low digit)
   w.rhist = (int32_t*)take((size_t)(B * RADIX_MAX_R * (w.n_sort_chunks + RADIX_MAX_R)) * 4);
   w.rbin = (int32_t*)take((size_t)B * RADIX_MAX_R * 4);
@@ -61,7 +67,8 @@ Workspace carve(void* base, int64_t B, int64_t N, int64_t D_user, int64_t K, int
   const bool tiled = assign_tiled(dt, D);
   w.keys = (uint64_t*)take(tiled ? (size_t)(B * N + 1) * 8 + TILED_ZERO_BYTES : 0);
   w.xnorm = (float*)take(tiled ? (size_t)(B * N) * 4 : 0);
-  const bool pad = D != D_user;
+  const bool pad = D != D_user || dt != dt_user;
+  w.copied = pad;
   w.xpad = take(pad ? (size_t)(B * N * D) * dt_bytes(dt) : 0);
   w.cpad = (float*)take(pad ? (size_t)(B * K * D) * 4 : 0);
   w.total = o;
@@ -80,7 +87,8 @@ static int check_sizes(int64_t B, int64_t N, int64_t D, int64_t K, int dt) {
 }
 
 // Points (and centroids, when given) into the workspace's zero-padded rows
-// when the kernels run at a wider row than D; the pointers the kernels read.
+// when the kernels run at a wider row than D (and, for narrow 16-bit rows,
+// widened to fp32); the pointers the kernels read.
 struct KernelArgs {
   const void* X;
   float* C;
@@ -90,8 +98,10 @@ static hipError_t pad_inputs(const void* X, const float* C, int dt, const Worksp
                              hipStream_t s) {
   a->X = X;
   a->C = const_cast<float*>(C);
-  if (w.Dk == D) return hipSuccess;
-  hipError_t e = launch_pad_rows(X, B * N, D, w.Dk, dt_bytes(dt), w.xpad, s);
+  if (!w.copied) return hipSuccess;
+  hipError_t e = w.kdt != dt
+                     ? launch_widen_rows(X, dt, B * N, D, w.Dk, (float*)w.xpad, s)
+                     : launch_pad_rows(X, B * N, D, w.Dk, dt_bytes(dt), w.xpad, s);
   if (e == hipSuccess && C) e = launch_pad_rows(C, B * K, D, w.Dk, 4, w.cpad, s);
   a->X = w.xpad;
   a->C = w.cpad;
@@ -154,8 +164,8 @@ int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t 
   const Workspace w = carve(ws, B, N, D, K, xdtype);
   KernelArgs a;
   if ((rc = hip_status(pad_inputs(X, C, xdtype, w, B, N, D, K, &a, s)))) return rc;
-  if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, w.Dk, w.chat, w.cinit, s)))) return rc;
-  return hip_status(launch_assign(a.X, xdtype, w, B, N, w.Dk, K, idx, min_dist, s));
+  if ((rc = hip_status(launch_prep(a.C, w.kdt, B, K, w.Kp, w.Dk, w.chat, w.cinit, s)))) return rc;
+  return hip_status(launch_assign(a.X, w.kdt, w, B, N, w.Dk, K, idx, min_dist, s));
 }
 
 int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_prev, int64_t B,
@@ -170,12 +180,12 @@ int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_
   const Workspace w = carve(ws, B, N, D, K, xdtype);
   KernelArgs a;
   if ((rc = hip_status(pad_inputs(X, C_prev, xdtype, w, B, N, D, K, &a, s)))) return rc;
-  if (w.Dk == D)
+  if (!w.copied)
     return hip_status(
         launch_update(X, xdtype, idx, C_prev, w, B, N, D, K, C_out, counts, NextStep{}, s));
-  // padded rows: update the padded copy in place, then write its first D columns
+  // copied rows: update the copy in place, then write its first D columns
   if ((rc = hip_status(
-           launch_update(a.X, xdtype, idx, a.C, w, B, N, w.Dk, K, a.C, counts, NextStep{}, s))))
+           launch_update(a.X, w.kdt, idx, a.C, w, B, N, w.Dk, K, a.C, counts, NextStep{}, s))))
     return rc;
   return hip_status(launch_unpad_rows(a.C, B * K, w.Dk, D, C_out, s));
 }
@@ -196,37 +206,38 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   KernelArgs a;
   if ((rc = hip_status(pad_inputs(X, C, xdtype, w, B, N, D, K, &a, s)))) return rc;
   const int64_t Dk = w.Dk;
+  const int kdt = w.kdt;
   // Small K: one kernel assigns and sums (X read once per iteration), with
   // the arithmetic of the kernels kmeans_assign and kmeans_update run for
   // these shapes; their workgroups take SMALLK_CH points each.
-  const bool fused = fused_ok(xdtype, Dk, K);
+  const bool fused = fused_ok(kdt, Dk, K);
   // The update's last kernel also writes the next iteration's rounded
   // centroids and scores (prep runs once) and this iteration's objective.
   NextStep nx;
-  nx.dt = xdtype;
+  nx.dt = kdt;
   nx.chat = w.chat;
   nx.cinit = w.cinit;
   nx.Kp = w.Kp;
   nx.objpart = w.objpart;
-  nx.nparts = sums_ok(xdtype, Dk, K) ? w.n_sk_chunks : w.n_assign_blocks;
+  nx.nparts = sums_ok(kdt, Dk, K) ? w.n_sk_chunks : w.n_assign_blocks;
   nx.iters = iters;
   nx.objective = objective;
-  if ((rc = hip_status(launch_prep(a.C, xdtype, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
+  if ((rc = hip_status(launch_prep(a.C, kdt, B, K, w.Kp, Dk, w.chat, w.cinit, s)))) return rc;
   for (int t = 0; t < iters; ++t) {
     nx.t = t;
     if (t + 1 == iters) nx.chat = nullptr;  // no next iteration
     if (fused)
-      rc = hip_status(launch_sums(a.X, xdtype, w, B, N, Dk, K, SUMS_FUSED, idx, min_dist, s));
+      rc = hip_status(launch_sums(a.X, kdt, w, B, N, Dk, K, SUMS_FUSED, idx, min_dist, s));
     else
-      rc = hip_status(launch_assign(a.X, xdtype, w, B, N, Dk, K, idx, min_dist, s));
+      rc = hip_status(launch_assign(a.X, kdt, w, B, N, Dk, K, idx, min_dist, s));
     if (rc) return rc;
     if (fused)
       rc = hip_status(launch_combine(w, w.n_sk_chunks, a.C, B, K, Dk, a.C, counts, nx, s));
     else
-      rc = hip_status(launch_update(a.X, xdtype, idx, a.C, w, B, N, Dk, K, a.C, counts, nx, s));
+      rc = hip_status(launch_update(a.X, kdt, idx, a.C, w, B, N, Dk, K, a.C, counts, nx, s));
     if (rc) return rc;
   }
-  if (Dk != D) return hip_status(launch_unpad_rows(a.C, B * K, Dk, D, C, s));
+  if (w.copied) return hip_status(launch_unpad_rows(a.C, B * K, Dk, D, C, s));
   return FKM_OK;
 }
 

@@ -285,6 +285,34 @@ hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk,
   return hipGetLastError();
 }
 
+template <int DT>
+__global__ __launch_bounds__(256) void widen_rows_kernel(const uint16_t* __restrict__ src,
+                                                         int64_t rows, int Din, int Dout,
+                                                         float* __restrict__ dst) {
+  const int64_t r0 = (int64_t)blockIdx.x * PAD_ROWS;
+  const int64_t left = rows - r0;
+  const int nr = left < PAD_ROWS ? (int)left : PAD_ROWS;
+  src += r0 * Din;
+  dst += r0 * Dout;
+  const unsigned total = (unsigned)nr * (unsigned)Dout;
+  for (unsigned j = threadIdx.x; j < total; j += 256) {
+    const unsigned r = j / (unsigned)Dout, d = j - r * (unsigned)Dout;
+    dst[j] = (int)d < Din ? Elem<DT>::widen(src[(size_t)r * Din + d]) : 0.f;
+  }
+}
+
+hipError_t launch_widen_rows(const void* src, int dt, int64_t rows, int64_t D, int64_t Dk,
+                             float* dst, hipStream_t s) {
+  const dim3 grid((unsigned)((rows + PAD_ROWS - 1) / PAD_ROWS));
+  if (dt == DT_BF16)
+    widen_rows_kernel<DT_BF16><<<grid, 256, 0, s>>>((const uint16_t*)src, rows, (int)D, (int)Dk, dst);
+  else if (dt == DT_F16)
+    widen_rows_kernel<DT_F16><<<grid, 256, 0, s>>>((const uint16_t*)src, rows, (int)D, (int)Dk, dst);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
                              hipStream_t s) {
   const dim3 grid((unsigned)((rows + PAD_ROWS - 1) / PAD_ROWS));

@@ -43,8 +43,8 @@ namespace fkm {
 // masked value keeps the earliest tile.  Scores within 16 ulp of each other
 // therefore count as ties and go to the lowest index; nothing else changes.
 // Since |s'| is up to about Q, that window (and the error of min_dist) is
-// relative to the workgroup's largest norm; rows of 16 elements subtract each
-// point's own bound instead (below).
+// relative to the workgroup's largest norm; a workgroup whose points' norms
+// spread widely subtracts each point's own bound instead (below).
 // Padding rows score -FLT_MAX (an infinity with position bits would be a
 // signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
 typedef __attribute__((address_space(1))) void global_void;
@@ -203,49 +203,43 @@ __device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB
   __syncthreads();
 }
 
-template <int DT, int CPL, int NSUB>
-__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
-    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
-    int N, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
-    double* __restrict__ objpart) {
-  static_assert(DT != DT_F32, "16-bit storage types only");
+// Largest ratio of squared point norms within a workgroup for which one
+// shift serves all its points: the 16-ulp tie window and the rounding of
+// min_dist then stay below 2^-19 * 64 = 2^-13 of each point's |x|^2.  A
+// workgroup with a wider spread is left to assign_pipe_wide_kernel, which
+// shifts each point by its own bound.
+constexpr float PIPE_WIDE_RATIO = 64.f;
+
+// One workgroup's block of PPB points against all centroids.  PPQ = false:
+// the workgroup's shift Q is folded into the stored scores (no cost per
+// tile); a block whose squared norms spread by more than PIPE_WIDE_RATIO is
+// only flagged (wide[blk] = 1) and left alone.  PPQ = true: each point's own
+// shift, subtracted in the epilogue (16 subtractions per tile and point tile).
+template <int DT, int CPL, int NSUB, bool PPQ>
+__device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
+                                           const u32x4* __restrict__ chat4,
+                                           const float* __restrict__ cinit, int N, int nst,
+                                           int32_t* __restrict__ idx, float* __restrict__ min_dist,
+                                           double* __restrict__ objpart, int32_t* __restrict__ wide,
+                                           char* buf0, char* buf1, float* lds_q, float* lds_qmin,
+                                           double* lds_obj) {
   using L = PipeLayout<CPL>;
-  static_assert(ASSIGN_KPAD % L::TCS == 0, "K is padded to whole stages");
   constexpr int RC = L::RC;
   constexpr int PPW = 32 * NSUB;           // points per wave
   constexpr int PPB = 4 * PPW;             // points per workgroup
   constexpr int LOADS = L::TCS * L::RCP / ASSIGN_THREADS;
-  static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * L::RCP, "stage must split evenly");
-  // Rows of 16 elements shift each point's scores by its own bound: their
-  // norms spread too widely for one shift per workgroup (the 16-ulp tie window
-  // would be wide against the smallest points' distances).  Wider rows take
-  // the workgroup's shift, folded into the stored scores at no cost per tile.
-  constexpr bool PPQ = CPL == 1;
-
-  __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
-  __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
-  __shared__ float lds_q[4];
-  __shared__ double lds_obj[4];
-
-  const int b = blockIdx.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
-  X += (size_t)b * N * RC;
-  const u32x4* chat4 = reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * RC;
-  cinit += (size_t)b * Kp;
-  idx += (size_t)b * N;
-  min_dist += (size_t)b * N;
-  const int nst = Kp / L::TCS;
 
   PipeOffsets<CPL, LOADS> o;
   pipe_offsets<CPL, LOADS>(o, tid, n, h);
   const float n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
 
-  const int pbase = blockIdx.x * PPB + wave * PPW;
+  const int pbase = blk * PPB + wave * PPW;
   uint4 xr[NSUB][CPL];
   float xn[NSUB];
-  float xmax = 0.f;
+  float xmax = 0.f, xmin = __builtin_inff();
 #pragma unroll
   for (int p = 0; p < NSUB; ++p) {
     const int pt = pbase + p * 32 + n;
@@ -259,19 +253,38 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
     ss += __shfl_xor(ss, 32);
     xn[p] = ss;
     xmax = __builtin_fmaxf(xmax, ss);
+    xmin = ok ? __builtin_fminf(xmin, ss) : xmin;  // points past N do not count
   }
+  float Q = 0.f;
+  if constexpr (!PPQ) {
 #pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) xmax = __builtin_fmaxf(xmax, __shfl_xor(xmax, msk));
-  if (lane == 0) lds_q[wave] = xmax;
-  __syncthreads();
-  // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding);
-  // with PPQ each point's own |x|^2 / 2 (the same margin) and Q = 0
+    for (int msk = 1; msk < 64; msk <<= 1) {
+      xmax = __builtin_fmaxf(xmax, __shfl_xor(xmax, msk));
+      xmin = __builtin_fminf(xmin, __shfl_xor(xmin, msk));
+    }
+    if (lane == 0) {
+      lds_q[wave] = xmax;
+      lds_qmin[wave] = xmin;
+    }
+    __syncthreads();
+    const float wmax =
+        __builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3]));
+    const float wmin = __builtin_fminf(__builtin_fminf(lds_qmin[0], lds_qmin[1]),
+                                       __builtin_fminf(lds_qmin[2], lds_qmin[3]));
+    // the same value in every thread (from LDS after a barrier): a uniform branch
+    const bool spread = wmax > PIPE_WIDE_RATIO * wmin;
+    if (tid == 0) wide[blk] = spread ? 1 : 0;
+    if (spread) {
+      __builtin_amdgcn_s_waitcnt(0);  // the first stage's loads into LDS complete before exit
+      return;
+    }
+    // Q >= max |x|^2 / 2 with a relative margin of 2^-8 (far above fp32 rounding)
+    Q = __builtin_fmaf(0.5f * wmax, 1.0f + 0x1p-8f, 1e-30f);
+  }
+  // per point: its own |x|^2 / 2 with the same margin (used when PPQ)
   float Qp[NSUB];
 #pragma unroll
   for (int p = 0; p < NSUB; ++p) Qp[p] = __builtin_fmaf(0.5f * xn[p], 1.0f + 0x1p-8f, 1e-30f);
-  const float Q = PPQ ? 0.f : __builtin_fmaf(
-      0.5f * __builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])),
-      1.0f + 0x1p-8f, 1e-30f);
 
   float best[NSUB];
   uint32_t code[NSUB];
@@ -328,26 +341,90 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
   for (int msk = 1; msk < 64; msk <<= 1) obj += __shfl_xor(obj, msk);
   if (lane == 0) lds_obj[wave] = obj;
   __syncthreads();
-  if (tid == 0)
-    objpart[(size_t)b * gridDim.x + blockIdx.x] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
+  if (tid == 0) objpart[blk] = ((lds_obj[0] + lds_obj[1]) + lds_obj[2]) + lds_obj[3];
 }
+
+// The assignment of one block of points per workgroup with the workgroup's
+// shift; blocks whose norms spread widely are flagged in `wide` (per
+// instance, one int per block) and left to assign_pipe_wide_kernel.
+template <int DT, int CPL, int NSUB>
+__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
+    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
+    int N, int Kp, int32_t* __restrict__ idx, float* __restrict__ min_dist,
+    double* __restrict__ objpart, int32_t* __restrict__ wide) {
+  static_assert(DT != DT_F32, "16-bit storage types only");
+  static_assert(CPL >= 2, "16-bit rows of 16 elements run on the fp32 kernel");
+  using L = PipeLayout<CPL>;
+  static_assert(ASSIGN_KPAD % L::TCS == 0, "K is padded to whole stages");
+  static_assert(L::TCS * L::RCP / ASSIGN_THREADS * ASSIGN_THREADS == L::TCS * L::RCP,
+                "stage must split evenly");
+  __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
+  __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
+  __shared__ float lds_q[4], lds_qmin[4];
+  __shared__ double lds_obj[4];
+  const int b = blockIdx.y, nblk = gridDim.x;
+  pipe_block<DT, CPL, NSUB, false>(
+      blockIdx.x, X + (size_t)b * N * L::RC,
+      reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * L::RC, cinit + (size_t)b * Kp, N,
+      Kp / L::TCS, idx + (size_t)b * N, min_dist + (size_t)b * N, objpart + (size_t)b * nblk,
+      wide + (size_t)b * nblk, buf0, buf1, lds_q, lds_qmin, lds_obj);
+}
+
+// The flagged blocks, each point shifted by its own bound.  A fixed grid of
+// workgroups walks the blocks (block blockIdx.x, then every gridDim.x-th) and
+// skips the unflagged ones, so with no wide block it costs one read of the
+// flags.
+template <int DT, int CPL, int NSUB>
+__global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_wide_kernel(
+    const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
+    int N, int Kp, int nblk, int32_t* __restrict__ idx, float* __restrict__ min_dist,
+    double* __restrict__ objpart, const int32_t* __restrict__ wide) {
+  using L = PipeLayout<CPL>;
+  __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
+  __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
+  __shared__ double lds_obj[4];
+  const int b = blockIdx.y;
+  const int32_t* wb = wide + (size_t)b * nblk;
+  for (int blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
+    if (wb[blk] == 0) continue;  // one address for the whole workgroup: uniform
+    pipe_block<DT, CPL, NSUB, true>(
+        blk, X + (size_t)b * N * L::RC,
+        reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * L::RC, cinit + (size_t)b * Kp, N,
+        Kp / L::TCS, idx + (size_t)b * N, min_dist + (size_t)b * N, objpart + (size_t)b * nblk,
+        nullptr, buf0, buf1, nullptr, nullptr, lds_obj);
+    __syncthreads();  // every wave is done with the stage buffers before the next block
+  }
+}
+
+// Workgroups of the wide-block pass, over all instances: enough to cover a
+// few flagged blocks per CU, few enough that reading the flags is cheap when
+// none is set.
+constexpr int64_t PIPE_WIDE_GRID = 512;
 
 template <int DT, int CPL, int NSUB>
 hipError_t launch_pipe(const void* X, const Workspace& w, int64_t B, int64_t N,
                               int32_t* idx, float* min_dist, hipStream_t s) {
   const dim3 grid((unsigned)w.n_assign_blocks, (unsigned)B), block(ASSIGN_THREADS);
   assign_pipe_kernel<DT, CPL, NSUB><<<grid, block, 0, s>>>(
-      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)w.Kp, idx, min_dist, w.objpart);
+      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)w.Kp, idx, min_dist, w.objpart,
+      w.wide);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t per = (PIPE_WIDE_GRID + B - 1) / B;  // workgroups per instance
+  const int64_t nw = w.n_assign_blocks < per ? w.n_assign_blocks : per;
+  assign_pipe_wide_kernel<DT, CPL, NSUB><<<dim3((unsigned)nw, (unsigned)B), block, 0, s>>>(
+      (const uint4*)X, (const uint4*)w.chat, w.cinit, (int)N, (int)w.Kp, (int)w.n_assign_blocks,
+      idx, min_dist, w.objpart, w.wide);
   return hipGetLastError();
 }
 
-// CPL = D / 16 chunks per lane; NSUB must agree with assign_nsub16(D).
+// CPL = D / 16 chunks per lane (2 .. 16: 16-bit rows of 16 run as fp32);
+// NSUB must agree with assign_nsub16(D).
 template <int DT>
 hipError_t launch_pipe_dt(const void* X, const Workspace& w, int64_t B, int64_t N,
                                  int64_t D, int32_t* idx, float* min_dist, hipStream_t s) {
   if (D % 16 != 0) return hipErrorInvalidValue;
   switch (D / 16) {
-    case 1: return launch_pipe<DT, 1, 4>(X, w, B, N, idx, min_dist, s);
     case 2: return launch_pipe<DT, 2, 4>(X, w, B, N, idx, min_dist, s);
     case 3: return launch_pipe<DT, 3, 4>(X, w, B, N, idx, min_dist, s);
     case 4: return launch_pipe<DT, 4, 4>(X, w, B, N, idx, min_dist, s);

@@ -21,20 +21,23 @@
 // barrier sits in the middle of a stage: the second 16-dimension step's
 // MFMAs run after it, beside the reads of the next stage's first fragments.
 //
-// Scores.  As in the resident kernel, the accumulator starts at
-// -|c^|^2/2 - Q, with Q a bound on |x|^2/2 over the workgroup's 256 points
-// (from a row-norm pass) plus a margin, so every score is negative and the
-// packed-key epilogue applies: the lane's position j in the tile goes into the
-// 4 low mantissa bits, a max3 tree picks the tile's best, and a strict compare
-// on the masked value keeps the earliest tile (scores within 16 ulp count as
-// ties and go to the lowest index).  The two waves sharing a point range merge
+// Scores.  The accumulator of point p and centroid c starts at
+// -|c^|^2/2 - Q_p, with Q_p a bound on the point's own |x_p|^2/2 (from a
+// row-norm pass) plus a margin, so every score is negative and the packed-key
+// epilogue applies: the lane's position j in the tile goes into the 4 low
+// mantissa bits, a max3 tree picks the tile's best, and a strict compare on
+// the masked value keeps the earliest tile (scores within 16 ulp count as
+// ties and go to the lowest index).  The shift is per point, so that window
+// is relative to each point's own norm and distance, whatever the norms of
+// the other points in the workgroup; it costs 16 subtractions per tile and
+// block, against 2 D / 16 MFMAs.  The two waves sharing a point range merge
 // through LDS at the end, and the workgroup merges its result into a
 // per-point 64-bit key with atomicMax: the masked score mapped to an
 // order-preserving unsigned integer in the high half and the complemented
 // index in the low half, so the maximum is the largest score and, among equal
-// scores, the lowest index, whatever order the workgroups finish in.  Q
-// depends only on the point block, so every workgroup of a point block uses
-// the same Q, and the decode pass recomputes it the same way.
+// scores, the lowest index, whatever order the workgroups finish in.  Q_p
+// depends only on the point's norm, so every workgroup uses the same Q_p for
+// a point, and the decode pass recomputes it the same way.
 //
 // Blocks of D.  A block of centroids takes nds = D / 32 stages, padded to a
 // multiple of four (the buffer rotation).  A padding stage reloads the block's
@@ -94,10 +97,10 @@ __device__ __forceinline__ float unordered(uint32_t u) {
   return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
 }
 
-// Q >= max |x|^2 / 2 over a point block, with a relative margin of 2^-8; the
-// same bits wherever it is computed from the same norms.
-__device__ __forceinline__ float block_q(float xmax) {
-  return __builtin_fmaf(0.5f * xmax, 1.0f + 0x1p-8f, 1e-30f);
+// Q_p >= |x_p|^2 / 2 with a relative margin of 2^-8; the same bits wherever
+// it is computed from the same norm.
+__device__ __forceinline__ float point_q(float xn) {
+  return __builtin_fmaf(0.5f * xn, 1.0f + 0x1p-8f, 1e-30f);
 }
 
 template <typename T>
@@ -172,9 +175,10 @@ __device__ __forceinline__ void tiled_mfma(f32x16 (&acc)[4][TCW], const TiledFra
     for (int tc = 0; tc < TCW; ++tc) acc[tp][tc] = mfma32_chunk<DT>(f.a[tc], f.b[tp], acc[tp][tc]);
 }
 
-// A new block: every accumulator starts at its centroid's -|c^|^2/2 - Q.
+// A new block: the accumulator of point tile tp starts at its centroid's
+// -|c^|^2/2 minus the lane's point's Q_p.
 __device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][TCW], char* buf, int wc, int h,
-                                           float Q) {
+                                           const float (&Qp)[4]) {
 #pragma unroll
   for (int tc = 0; tc < TCW; ++tc) {
     f32x16 cin;
@@ -182,13 +186,15 @@ __device__ __forceinline__ void tiled_init(f32x16 (&acc)[4][TCW], char* buf, int
     for (int q = 0; q < 4; ++q) {
       const f32x4 v =
           lds_at<f32x4>(buf, XB + CB + (wc * 32 * TCW + tc * 32 + 8 * q + 4 * h) * 4);
-      cin[4 * q + 0] = v[0] - Q;
-      cin[4 * q + 1] = v[1] - Q;
-      cin[4 * q + 2] = v[2] - Q;
-      cin[4 * q + 3] = v[3] - Q;
+      cin[4 * q + 0] = v[0];
+      cin[4 * q + 1] = v[1];
+      cin[4 * q + 2] = v[2];
+      cin[4 * q + 3] = v[3];
     }
 #pragma unroll
-    for (int tp = 0; tp < 4; ++tp) acc[tp][tc] = cin;
+    for (int tp = 0; tp < 4; ++tp)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc[tp][tc][j] = cin[j] - Qp[tp];
   }
 }
 
@@ -259,7 +265,6 @@ __global__ __launch_bounds__(TT, 1) void assign_tiled_kernel(
   __shared__ __attribute__((aligned(16))) char buf1[STAGE];
   __shared__ __attribute__((aligned(16))) char buf2[STAGE];
   __shared__ __attribute__((aligned(16))) char buf3[STAGE];
-  __shared__ float lds_q[8];
 
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
@@ -298,11 +303,13 @@ __global__ __launch_bounds__(TT, 1) void assign_tiled_kernel(
   c.wp = wp;
   c.wc = wc;
 
-  // Q of the point block (waves 0 .. 3 hold its 256 norms)
-  float xm = tid < BP && tid <= c.last ? xnorm[(size_t)b * N + p0 + tid] : 0.f;
+  // Q_p of the lane's four points (column n of point tile tp)
+  float Qp[4];
 #pragma unroll
-  for (int m = 1; m < 64; m <<= 1) xm = __builtin_fmaxf(xm, __shfl_xor(xm, m));
-  if (lane == 0) lds_q[wave] = xm;
+  for (int tp = 0; tp < 4; ++tp) {
+    const int r = wp * 128 + tp * 32 + n;
+    Qp[tp] = point_q(r <= c.last ? xnorm[(size_t)b * N + p0 + r] : 0.f);
+  }
 
   // stages 0 .. 2 in flight before the loop; stage 0 complete
   const int S = c.S;
@@ -312,8 +319,6 @@ __global__ __launch_bounds__(TT, 1) void assign_tiled_kernel(
   if (2 < S) wait_loads_and_sync<2 * LOADS>();
   else if (1 < S) wait_loads_and_sync<LOADS>();
   else wait_loads_and_sync<0>();
-  const float Q =
-      block_q(__builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])));
 
   f32x16 acc[4][TCW];
   float best[4];
@@ -327,7 +332,7 @@ __global__ __launch_bounds__(TT, 1) void assign_tiled_kernel(
   tiled_read(f0, buf0, c.loff0, wp, wc);
   const int nq = ndsv / 4;  // every block starts in buffer 0
   for (int g = 0; g < ncbw; ++g) {
-    tiled_init(acc, buf0, wc, h, Q);
+    tiled_init(acc, buf0, wc, h, Qp);
     const int s0 = g * ndsv;
     const int full = g == ncbw - 1 ? nq - 1 : nq;  // quads with no stage past the end
     for (int q = 0; q < full; ++q)
@@ -404,32 +409,23 @@ __global__ __launch_bounds__(256) void fill_keys_kernel(uint64_t* __restrict__ k
   if (i < n) keys[i] = 0;
 }
 
-// idx, min_dist and per-block objective partials from the keys; a decode
-// block is a point block of the tiled kernel, so Q is recomputed from the
-// same norms.
+// idx, min_dist and per-block objective partials from the keys; each point's
+// Q_p is recomputed from the same norm.
 __global__ __launch_bounds__(256) void decode_keys_kernel(const uint64_t* __restrict__ keys,
                                                           const float* __restrict__ xnorm, int N,
                                                           int32_t* __restrict__ idx,
                                                           float* __restrict__ min_dist,
                                                           double* __restrict__ objpart) {
   __shared__ double s[256];
-  __shared__ float lds_q[4];
   const int b = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63;
+  const int t = threadIdx.x;
   const int i = blockIdx.x * 256 + t;
   const float xn = i < N ? xnorm[(size_t)b * N + i] : 0.f;
-  float xm = xn;
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) xm = __builtin_fmaxf(xm, __shfl_xor(xm, m));
-  if (lane == 0) lds_q[t >> 6] = xm;
-  __syncthreads();
-  const float Q =
-      block_q(__builtin_fmaxf(__builtin_fmaxf(lds_q[0], lds_q[1]), __builtin_fmaxf(lds_q[2], lds_q[3])));
   double md = 0.0;
   if (i < N) {
     const uint64_t key = keys[(size_t)b * N + i];
     const float v = unordered((uint32_t)(key >> 32));
-    const float d = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Q, xn), 0.f);
+    const float d = __builtin_fmaxf(__builtin_fmaf(-2.f, v + point_q(xn), xn), 0.f);
     idx[(size_t)b * N + i] = (int32_t)(0xffffffffu - (uint32_t)key);
     min_dist[(size_t)b * N + i] = d;
     md = d;

@@ -117,6 +117,14 @@ inline int64_t kernel_dim(int dt, int64_t D) {
   const int64_t Dk = D <= 256 ? (D + 15) / 16 * 16 : (D + 31) / 32 * 32;
   return row_bytes_ok(dt, Dk) && assign_ok(dt, Dk) ? Dk : 0;
 }
+// The storage type the kernels run in: the caller's, except for 16-bit rows
+// of at most 16 elements, which run as fp32 on widened (exact) copies.
+// Their centroids then enter the distances unrounded: rounding a centroid to
+// the 16-bit type moves a distance by about 2 <x - c, c - c^>, at most
+// 2 |x - c| 2^-9 |c| for bf16, which averages out over many dimensions but
+// over a handful is not small against 1e-3 |x|^2 when a point's nearest
+// centroids are far from it relative to its norm.
+inline int kernel_dt(int dt, int64_t D) { return dt != DT_F32 && D <= 16 ? DT_F32 : dt; }
 // Tiled kernel: 256 points x 256-centroid blocks, TILED_CBG blocks per
 // workgroup; its centroids are padded to whole blocks.
 constexpr int TILED_BP = 256, TILED_BC = 256, TILED_CBG = 8;
@@ -130,6 +138,7 @@ struct Workspace {
   void* chat;      // [B,Kp,D] centroids rounded to the storage type (Kp = kpad_for(dt, D, K))
   float* cinit;    // [B,Kp]   -1/2 * squared norm of each rounded centroid
   double* objpart; // [B,n_assign_blocks] per-workgroup objective partials
+  int32_t* wide;   // [B,n_assign_blocks] blocks whose norms spread widely (16-bit streaming assignment)
   int32_t* rhist;  // [B,R,chunks] radix histograms, then run starts (R <= 256; chunks <= n_sort_chunks + 256)
   int32_t* rbin;   // [B,256] radix bin totals
   int32_t* rbin1;  // [B,256] the first pass's bin totals (packed two-pass sort)
@@ -145,9 +154,11 @@ struct Workspace {
   int32_t* pcount; // [B,nch,K] per-chunk cluster counts
   uint64_t* keys;  // [B,N] best (score, index) of each point, then TILED_ZERO_BYTES of zeros (tiled assignment only)
   float* xnorm;    // [B,N] squared norms of the points (tiled assignment only)
-  void* xpad;      // [B,N,Dk] the points in zero-padded rows (only when Dk != D)
-  float* cpad;     // [B,K,Dk] the centroids in zero-padded rows (only when Dk != D)
+  void* xpad;      // [B,N,Dk] the points in zero-padded rows of type kdt (only when copied)
+  float* cpad;     // [B,K,Dk] the centroids in zero-padded rows (only when copied)
   int64_t Dk;      // the row width the kernels run at (kernel_dim)
+  int kdt;         // the storage type the kernels run in (kernel_dt)
+  bool copied;     // the kernels read copies (xpad, cpad): Dk != D or kdt != the caller's type
   int64_t Kp, n_assign_blocks, n_sort_chunks, n_red_chunks, red_cr, n_sk_chunks;
   size_t total;
 };
@@ -202,6 +213,9 @@ hipError_t launch_assign_tiled(const void* X, int dt, const Workspace& w, int64_
                                int64_t D, int32_t* idx, float* min_dist, hipStream_t s);
 hipError_t launch_pad_rows(const void* src, int64_t rows, int64_t D, int64_t Dk, int elem_bytes,
                            void* dst, hipStream_t s);
+// 16-bit rows of D elements (dt) into fp32 rows of Dk >= D (zeros past D).
+hipError_t launch_widen_rows(const void* src, int dt, int64_t rows, int64_t D, int64_t Dk,
+                             float* dst, hipStream_t s);
 hipError_t launch_unpad_rows(const float* src, int64_t rows, int64_t Dk, int64_t D, float* dst,
                              hipStream_t s);
 hipError_t update_init();

@@ -19,6 +19,10 @@ Recipe (one line per workload, base seeds fixed below):
 * initial centroids: the first K points (``init="first"``) or a seeded sample
   of K distinct points in draw order (``init="sample"``), widened exactly to
   fp32.
+* ``make_multiscale`` (a test input, not a benchmark workload): blob points
+  as above, each multiplied by its own scale drawn log-uniformly from
+  ``[1, ratio]``, so that points whose squared norms differ by up to
+  ``ratio^2`` sit side by side in every block of consecutive rows.
 
 Every random stream comes from ``numpy.random.SeedSequence(base).spawn``; the
 noise is drawn in fixed row chunks, each from its own spawned stream, so the
@@ -34,7 +38,7 @@ from typing import Optional
 import numpy as np
 import torch
 
-__all__ = ["WORKLOADS", "Workload", "make_workload", "raw_bits", "DTYPES"]
+__all__ = ["WORKLOADS", "Workload", "make_workload", "make_multiscale", "raw_bits", "DTYPES"]
 
 DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
 
@@ -193,6 +197,40 @@ def make_workload(cfg: int, *, N: Optional[int] = None, K: Optional[int] = None,
     return Workload(name=name, B=B, N=N, D=D, K=K, dtype=spec["dtype"], iters=spec["iters"],
                     X=X, C0=C0, labels=labels,
                     centres=np.stack(centres) if centres else None, spec=spec)
+
+
+def make_multiscale(B: int, N: int, D: int, K: int, dtype: str, *, ratio: float = 100.0,
+                    n_blobs: int = 64, sigma: float = 0.15, seed: int = 0x2608_00F0) -> Workload:
+    """Blob points with per-point scales spread over ``[1, ratio]`` (log-uniform).
+
+    x = s * (centre[label] + sigma * N(0, I)) in fp32, s = ratio ** u with
+    u ~ U[0, 1), then one RNE cast; centroids are a seeded sample of K points.
+    Consecutive rows mix all scales, so any block of a few hundred points holds
+    squared norms over about ``ratio^2``.
+    """
+    if K > N:
+        raise ValueError("K must not exceed N")
+    dt = DTYPES[dtype]
+    X = torch.empty((B, N, D), dtype=dt)
+    C0 = torch.empty((B, K, D), dtype=torch.float32)
+    labels = np.empty((B, N), np.int32)
+    for b, ss in enumerate(np.random.SeedSequence([seed, B, N, D, K]).spawn(B)):
+        s_centre, s_label, s_scale, s_noise, s_init = ss.spawn(5)
+        centres = np.random.default_rng(s_centre).uniform(-1, 1, size=(n_blobs, D)).astype(np.float32)
+        lab = np.random.default_rng(s_label).integers(0, n_blobs, size=N).astype(np.int32)
+        scale = (ratio ** np.random.default_rng(s_scale).random(N)).astype(np.float32)
+        x = np.random.default_rng(s_noise).standard_normal((N, D), dtype=np.float32)
+        x *= np.float32(sigma)
+        x += centres[lab]
+        x *= scale[:, None]
+        X[b].copy_(torch.from_numpy(x))
+        rows = np.random.default_rng(s_init).choice(N, size=K, replace=False)
+        C0[b] = X[b][torch.from_numpy(rows.astype(np.int64))].float()
+        labels[b] = lab
+    return Workload(name=f"multiscale_r{ratio:g}_b{B}_n{N}_d{D}_k{K}_{dtype}", B=B, N=N, D=D, K=K,
+                    dtype=dtype, iters=2, X=X, C0=C0, labels=labels, centres=None,
+                    spec=dict(kind="multiscale", ratio=ratio, n_blobs=n_blobs, sigma=sigma,
+                              seed=seed))
 
 
 def raw_bits(t: torch.Tensor) -> np.ndarray:

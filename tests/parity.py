@@ -2,7 +2,8 @@
 
 * assignments: identical, except points whose oracle gap (second-smallest minus
   smallest squared distance) is below 1e-3 * |x|^2; disagreements on those
-  points are counted and reported, never hidden.
+  points are counted and reported, never hidden, and the centroid chosen
+  there must itself lie within that window: d(x, c_gpu) - d_min <= 1e-3 * |x|^2.
 * min_dist: |gpu - d(x, c_gpu_idx)| <= tol * (|x|^2 + |c_gpu_idx|^2).
 * centroids: per centroid, |c_gpu - c_oracle| <= tol * |c_oracle| (norm-wise).
 * counts: identical.  objective: relative difference <= tol (with an absolute
@@ -62,6 +63,13 @@ def check_assign(o, X_raw, dtype, C64, idx_gpu, md_gpu) -> AssignReport:
         bi, ni = np.nonzero(bad)
         c = C64[bi, idx_gpu[bi, ni]]
         d_choice[bi, ni] = ((x64[bi, ni] - c) ** 2).sum(-1)
+        # an exempt disagreement must still pick a centroid inside the window
+        excess = d_choice[bi, ni] - md_o[bi, ni]
+        lim = GAP_REL * xn[bi, ni]
+        far = excess > lim
+        assert not far.any(), (f"{int(far.sum())} exempt mismatches chose a centroid outside the "
+                               f"1e-3*|x|^2 window, e.g. point {(bi[far][0], ni[far][0])}: "
+                               f"excess {excess[far][0]:.3e} > {lim[far][0]:.3e}")
     cn = (C64 ** 2).sum(-1)
     scale = xn + np.take_along_axis(cn, idx_gpu, axis=1)
     err = np.abs(md_gpu - d_choice) / np.maximum(scale, 1e-300)

@@ -34,15 +34,9 @@ def km():
     return kmeans
 
 
-def teacher_forced(km, o, X, C0, dtype, iters, rows=None, rounded=False):
-    """Run `iters` assign/update steps on the GPU and check each against the oracle.
-
-    rounded: check the assignment against the centroids rounded to the points'
-    type (torch's round-to-nearest-even cast), the ones the kernel measures
-    distances to.  Over D >= 16 dimensions the rounding errors average out far
-    below the tolerance; over a handful they need not (the bound is
-    2 |x - c| u |c| with u = 2^-8 for bf16), so narrow rows are checked this way.
-    """
+def teacher_forced(km, o, X, C0, dtype, iters, rows=None):
+    """Run `iters` assign/update steps on the GPU and check each against the oracle
+    (given the fp32 centroids the GPU was given)."""
     Xd = X.cuda()
     C = C0.cuda().clone()
     Xr = raw(X)
@@ -54,24 +48,18 @@ def teacher_forced(km, o, X, C0, dtype, iters, rows=None, rounded=False):
         C1, n = km.kmeans_update(Xd, idx, C, ws=ws)
         torch.cuda.synchronize()
         C64 = C.cpu().double().numpy()
-        Ca64 = C.cpu().to(X.dtype).double().numpy() if rounded else C64
         ig, mg = idx.cpu().numpy(), md.cpu().numpy()
         if rows is not None:
             ig_s, mg_s = ig[:, rows], mg[:, rows]
         else:
             ig_s, mg_s = ig, mg
-        rep = check_assign(o, Xs, dtype, Ca64, ig_s, mg_s) if rows is None else \
-            check_assign_rows(o, Xs, dtype, Ca64, ig_s, mg_s)
+        rep = check_assign(o, Xs, dtype, C64, ig_s, mg_s)
         err = check_update(o, Xr, dtype, ig, C64, C1.cpu().numpy(), n.cpu().numpy())
         say(f"  t={t} mismatches={rep.mismatches} (exempt pts {rep.exempt_points}) "
             f"md_err={rep.worst_md_err:.2e} J={rep.J_gpu:.6e}/{rep.J_oracle:.6e} C_err={err:.2e}")
         reports.append(rep)
         C = C1
     return reports
-
-
-def check_assign_rows(o, Xs, dtype, C64, ig, mg):
-    return check_assign(o, Xs, dtype, C64, ig, mg)
 
 
 # ----------------------------------------------------------------- workloads
@@ -147,7 +135,7 @@ SHAPES = [
     (1, 300, 64, 300, "bf16"),        # K = N
     (2, 6000, 128, 128, "bf16"),      # per-chunk update at K * D = 16384, ragged chunk
     (1, 10000, 32, 512, "f32"),       # per-chunk update, fp32, 9-bit cluster ids
-    (1, 3000, 16, 10, "bf16"),        # D = 16: one chunk per lane
+    (1, 3000, 16, 10, "bf16"),        # D = 16: 16-bit rows of <= 16 run as fp32
     (1, 4000, 32, 250, "bf16"),       # one-hot sums with 8 cluster tiles
     (1, 3000, 80, 60, "f16"),         # one-hot sums, odd chunk count (a padded dimension tile)
     (1, 3000, 48, 37, "f16"),         # D = 48: padded LDS rows, masked row lanes
@@ -168,7 +156,11 @@ SHAPES = [
     (2, 700, 1024, 33, "f16"),        # tiled kernel, batched
     (1, 300, 2048, 260, "bf16"),      # tiled kernel, widest rows
     # widths the kernels do not take run on zero-padded copies of the rows
-    (1, 1000, 1, 5, "bf16"),          # D = 1 -> 16
+    (1, 1000, 1, 5, "bf16"),          # D = 1: 16-bit rows below 16 run as fp32 rows of 16
+    (1, 3000, 1, 12, "f16"),          # D = 1, fp16
+    (1, 3000, 3, 8, "bf16"),          # D = 3, bf16
+    (2, 2000, 7, 30, "f16"),          # D = 7, batched
+    (1, 2500, 15, 300, "bf16"),       # D = 15, sorted update
     (1, 3000, 3, 8, "f32"),           # D = 3 -> 16
     (1, 3000, 40, 30, "bf16"),        # D = 40 -> 48
     (2, 1500, 100, 70, "f16"),        # D = 100 -> 112, batched
@@ -182,7 +174,38 @@ def test_edge_shapes(km, oracle, shape):
     B, N, D, K, dt = shape
     X, C0 = _blobs(B, N, D, K, DT[dt], seed=N * 7 + K)
     say(f"[edge] B={B} N={N} D={D} K={K} {dt}")
-    teacher_forced(km, oracle, X, C0, dt, 2, rounded=D < 16 and dt != "f32")
+    teacher_forced(km, oracle, X, C0, dt, 2)
+
+
+# Points whose squared norms differ by up to 10^4 in every workgroup: the
+# shift that keeps the packed scores negative must not widen the tie window or
+# the min_dist rounding past the smallest points' own tolerance.  Shapes cover
+# the streaming kernel (D = 64, 128; per-workgroup fallback to per-point
+# shifts), rows of 16 (always per point), the small-K single-pass kernel
+# (per point), the wide-row tiled kernel (per point) and fp32 rows.
+MULTISCALE = [
+    # (B, N, D, K, dtype)
+    (1, 20000, 64, 256, "bf16"),
+    (1, 20000, 128, 512, "bf16"),
+    (1, 20000, 128, 300, "f16"),
+    (1, 20000, 16, 200, "bf16"),
+    (2, 8192, 64, 64, "f16"),
+    (1, 6000, 1024, 300, "bf16"),
+    (1, 20000, 64, 256, "f32"),
+]
+
+
+@pytest.mark.parametrize("shape", MULTISCALE, ids=lambda s: "x".join(map(str, s)))
+def test_multiscale_norms(km, oracle, shape):
+    from paper_2608_12629_amd.synth import make_multiscale
+    B, N, D, K, dt = shape
+    w = make_multiscale(B, N, D, K, dt)
+    xn = (w.X.double() ** 2).sum(-1)
+    blk = xn[0, : (N // 256) * 256].reshape(-1, 256)
+    say(f"[multiscale] {w.name}: |x|^2 spread per 256 rows "
+        f"{float((blk.max(1).values / blk.min(1).values).min()):.0f}x or more")
+    assert float((blk.max(1).values / blk.min(1).values).min()) > 1e3
+    teacher_forced(km, oracle, w.X, w.C0, dt, 2)
 
 
 def test_duplicates_and_empty_clusters(km, oracle):
