@@ -70,7 +70,8 @@ typedef enum {
     FKM_ERR_INVALID_ARG = -1,  /* null pointer, size < 1, bad dtype, misaligned pointer, iters < 1 */
     FKM_ERR_UNSUPPORTED = -2,  /* see the limits above */
     FKM_ERR_WORKSPACE = -3,    /* ws NULL or ws_bytes smaller than kmeans_workspace_bytes() */
-    FKM_ERR_HIP = -4           /* a HIP runtime call or a kernel launch failed */
+    FKM_ERR_HIP = -4,          /* a HIP runtime call or a kernel launch failed */
+    FKM_ERR_SCRATCH = -5       /* kmeans_lloyd_noalloc: the workspace would exceed KMEANS_SCRATCH_BYTES */
 } fkm_status;
 
 /*
@@ -125,6 +126,25 @@ int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_
 int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D, int64_t K,
                  int iters, int32_t* idx, float* min_dist, int32_t* counts, double* objective,
                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kmeans_lloyd for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same computation and results as kmeans_lloyd, without the `ws` argument.
+ * Its workspace is a static device array of KMEANS_SCRATCH_BYTES (64 MiB)
+ * inside the library, one per GPU it runs on, held until the process ends;
+ * nothing is allocated by the call.  Problems whose kmeans_workspace_bytes()
+ * exceeds KMEANS_SCRATCH_BYTES are rejected with FKM_ERR_SCRATCH before any
+ * device work.  The caller still passes (and owns) the inputs and outputs.
+ * Every call on one GPU shares that GPU's array: calls that can overlap on one
+ * GPU (other streams, other host threads) race and must be serialized by the
+ * caller.  The first call on a device looks the array's address up once;
+ * make one call before capturing a graph.
+ */
+#define KMEANS_SCRATCH_BYTES ((size_t)64 << 20)
+int kmeans_lloyd_noalloc(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D,
+                         int64_t K, int iters, int32_t* idx, float* min_dist, int32_t* counts,
+                         double* objective, void* stream);
 
 /*
  * KNN search (paper Section 6 lists KNN search beside KMeans among its

@@ -4,6 +4,7 @@
 // the arguments have been validated.
 #include <atomic>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/flashkmeans.h"
 #include "fkm_internal.h"
@@ -141,6 +142,32 @@ static int check_device() {
 
 static int hip_status(hipError_t e) { return e == hipSuccess ? FKM_OK : FKM_ERR_HIP; }
 
+// The workspace of kmeans_lloyd_noalloc: a static device array, one per GPU,
+// alive until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+static_assert(KMEANS_SCRATCH_BYTES % 256 == 0, "whole 256-byte lines");
+__device__ __align__(256) char scratch[KMEANS_SCRATCH_BYTES];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[256];  // per device; nullptr until looked up
+
+// The device address of `scratch` on the current device (looked up on the
+// first call on each device).
+static int scratch_on_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FKM_ERR_HIP;
+  if (dev < 0 || dev >= 256) return FKM_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FKM_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FKM_OK;
+}
+
 }  // namespace fkm
 
 using namespace fkm;
@@ -241,6 +268,25 @@ int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int6
   return FKM_OK;
 }
 
+int kmeans_lloyd_noalloc(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D,
+                         int64_t K, int iters, int32_t* idx, float* min_dist, int32_t* counts,
+                         double* objective, void* stream) {
+  int rc;
+  if ((rc = check_ptrs({X, C, idx, min_dist, counts}))) return rc;
+  if (objective && !aligned16(objective)) return FKM_ERR_INVALID_ARG;
+  if (iters < 1) return FKM_ERR_INVALID_ARG;
+  if ((rc = check_sizes(B, N, D, K, xdtype))) return rc;
+  if (carve(nullptr, B, N, D, K, xdtype).total > KMEANS_SCRATCH_BYTES) return FKM_ERR_SCRATCH;
+  if ((rc = check_device())) return rc;
+  void* ws = nullptr;
+  if ((rc = scratch_on_device(&ws))) return rc;
+  // the same launch sequence as kmeans_lloyd, on the static array; every
+  // kernel writes its part of the workspace before reading it, so nothing
+  // needs clearing between calls
+  return kmeans_lloyd(X, xdtype, C, B, N, D, K, iters, idx, min_dist, counts, objective, ws,
+                      KMEANS_SCRATCH_BYTES, stream);
+}
+
 // ---- KNN search ---------------------------------------------------------------
 static int knn_check_sizes(int64_t B, int64_t M, int64_t N, int64_t D, int64_t k, int dt) {
   if (B < 1 || M < 1 || N < 1 || D < 1 || k < 1 || k > N) return FKM_ERR_INVALID_ARG;
@@ -313,6 +359,7 @@ const char* kmeans_status_string(int status) {
     case FKM_ERR_UNSUPPORTED: return "unsupported (device or shape outside this build)";
     case FKM_ERR_WORKSPACE: return "workspace missing or too small";
     case FKM_ERR_HIP: return "HIP runtime error";
+    case FKM_ERR_SCRATCH: return "problem needs more workspace than the static scratch array holds";
     default: return "unknown status";
   }
 }

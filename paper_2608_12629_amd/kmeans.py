@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libflashkmeans.so")
 
 F32, BF16, F16 = 0, 1, 2
 _DTYPE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCRATCH = 0, -1, -2, -3, -4, -5
+SCRATCH_BYTES = 64 << 20  # KMEANS_SCRATCH_BYTES
 
 
 class KMeansError(RuntimeError):
@@ -38,10 +39,12 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     lib.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     lib.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.kmeans_lloyd_noalloc.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp]
     lib.kmeans_knn_workspace_bytes.argtypes = [i64, i64, i64, i64, i32, i32]
     lib.kmeans_knn_workspace_bytes.restype = sz
     lib.kmeans_knn.argtypes = [vp, vp, i32, i64, i64, i64, i64, i32, vp, vp, vp, sz, vp]
-    for f in (lib.kmeans_assign, lib.kmeans_update, lib.kmeans_lloyd, lib.kmeans_knn):
+    for f in (lib.kmeans_assign, lib.kmeans_update, lib.kmeans_lloyd, lib.kmeans_lloyd_noalloc,
+              lib.kmeans_knn):
         f.restype = ctypes.c_int
     lib.kmeans_status_string.argtypes = [ctypes.c_int]
     lib.kmeans_status_string.restype = ctypes.c_char_p
@@ -182,6 +185,31 @@ def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
                             _ptr(min_dist), _ptr(counts), _ptr(obj), _ptr(ws.buf), ws.nbytes,
                             _stream()), "kmeans_lloyd")
     return C, idx, min_dist, counts, obj
+
+
+def kmeans_lloyd_noalloc(X: torch.Tensor, C: torch.Tensor, iters: int, idx: torch.Tensor,
+                         min_dist: torch.Tensor, counts: torch.Tensor,
+                         objective: Optional[torch.Tensor] = None):
+    """``kmeans_lloyd`` on the library's static scratch array: every output is
+    passed in, nothing is allocated (see ``kmeans_lloyd_noalloc`` in the header).
+    Returns (C, idx, min_dist, counts, objective)."""
+    B, N, D, K = _shapes(X, C)
+    _need(X, "X")
+    _need(C, "C", torch.float32)
+    for t, name, dt, shape in ((idx, "idx", torch.int32, (B, N)),
+                               (min_dist, "min_dist", torch.float32, (B, N)),
+                               (counts, "counts", torch.int32, (B, K))):
+        _need(t, name, dt)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, want {shape}")
+    if objective is not None:
+        _need(objective, "objective", torch.float64)
+        if tuple(objective.shape) != (B, iters):
+            raise ValueError(f"objective has shape {tuple(objective.shape)}, want {(B, iters)}")
+    _check(lib.kmeans_lloyd_noalloc(_ptr(X), _dt(X), _ptr(C), B, N, D, K, int(iters), _ptr(idx),
+                                    _ptr(min_dist), _ptr(counts), _ptr(objective), _stream()),
+           "kmeans_lloyd_noalloc")
+    return C, idx, min_dist, counts, objective
 
 
 def knn_workspace_bytes(B: int, M: int, N: int, D: int, k: int, dtype: torch.dtype) -> int:

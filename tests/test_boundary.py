@@ -10,7 +10,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "flashkmeans.h")
 LIB = os.path.join(ROOT, "paper_2608_12629_amd", "libflashkmeans.so")
 
-OK, EINVAL, EUNSUP, EWS, EHIP = 0, -1, -2, -3, -4
+OK, EINVAL, EUNSUP, EWS, EHIP, ESCRATCH = 0, -1, -2, -3, -4, -5
+SCRATCH_BYTES = 64 << 20
 F32, BF16, F16 = 0, 1, 2
 
 
@@ -31,6 +32,7 @@ def lib():
     L.kmeans_assign.argtypes = [vp, i32, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     L.kmeans_update.argtypes = [vp, i32, vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
     L.kmeans_lloyd.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.kmeans_lloyd_noalloc.argtypes = [vp, i32, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp]
     L.kmeans_knn_workspace_bytes.argtypes = [i64, i64, i64, i64, i32, i32]
     L.kmeans_knn_workspace_bytes.restype = sz
     L.kmeans_knn.argtypes = [vp, vp, i32, i64, i64, i64, i64, i32, vp, vp, vp, sz, vp]
@@ -41,8 +43,11 @@ def lib():
 
 def test_header_declares_the_calls():
     assert declared_functions() == ["kmeans_assign", "kmeans_knn", "kmeans_knn_workspace_bytes",
-                                    "kmeans_lloyd", "kmeans_status_string", "kmeans_update",
+                                    "kmeans_lloyd", "kmeans_lloyd_noalloc",
+                                    "kmeans_status_string", "kmeans_update",
                                     "kmeans_workspace_bytes"]
+    text = open(HEADER).read()
+    assert re.search(r"#define KMEANS_SCRATCH_BYTES \(\(size_t\)64 << 20\)", text)
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -51,7 +56,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for st in (OK, EINVAL, EUNSUP, EWS, EHIP):
+    for st in (OK, EINVAL, EUNSUP, EWS, EHIP, ESCRATCH):
         s = lib.kmeans_status_string(st).decode()
         assert s and s != "unknown status"
     assert lib.kmeans_status_string(12345).decode() == "unknown status"
@@ -152,6 +157,35 @@ def test_specific_rejections(lib):
     assert _lloyd(lib, obj=FAKE + 8) == EINVAL
     exact = lib.kmeans_workspace_bytes(1, 100, 64, 4, BF16)
     assert _assign(lib, wsb=exact - 1) == EWS
+
+
+def _noalloc(lib, X=FAKE, dt=BF16, C=FAKE, B=1, N=100, D=64, K=4, iters=3, idx=FAKE, md=FAKE,
+             n=FAKE, obj=None):
+    return lib.kmeans_lloyd_noalloc(X, dt, C, B, N, D, K, iters, idx, md, n, obj, None)
+
+
+def test_noalloc_rejections_before_any_device_call(lib):
+    """The static-scratch entry point validates like kmeans_lloyd and rejects
+    problems whose workspace exceeds the array, all before touching a GPU."""
+    assert _noalloc(lib, X=None) == EINVAL
+    assert _noalloc(lib, C=FAKE + 4) == EINVAL
+    assert _noalloc(lib, n=None) == EINVAL
+    assert _noalloc(lib, obj=FAKE + 8) == EINVAL
+    assert _noalloc(lib, iters=0) == EINVAL
+    assert _noalloc(lib, dt=3) == EINVAL
+    assert _noalloc(lib, D=4096) == EUNSUP
+    assert _noalloc(lib, K=70000) == EUNSUP
+    # the 8M-point workload needs ~138 MiB of workspace: too big for the array
+    assert lib.kmeans_workspace_bytes(1, 8_388_608, 128, 4096, BF16) > SCRATCH_BYTES
+    assert _noalloc(lib, N=8_388_608, D=128, K=4096) == ESCRATCH
+    # the largest N that fits, and the first that does not (fp32, D = 64, K = 256)
+    fits = lambda N: lib.kmeans_workspace_bytes(1, N, 64, 256, F32) <= SCRATCH_BYTES
+    lo, hi = 1, 1 << 28
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        lo, hi = (mid, hi) if fits(mid) else (lo, mid)
+    assert _noalloc(lib, dt=F32, N=hi, D=64, K=256) == ESCRATCH
+    assert fits(65536)   # the fp32 blob workload fits
 
 
 def test_binding_refuses_without_library(tmp_path, monkeypatch):
