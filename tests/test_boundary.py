@@ -222,3 +222,28 @@ def test_knn_rejections(lib):
                                                        ("k", 5), ("dt", BF16))])
     assert kw() > 0 and kw(k=33) == 0 and kw(dt=F32) == 0
     assert kw(N=1000) >= kw(N=100)
+
+
+def test_calibration_library_exports_its_header():
+    """libfkm_calib.so (the benchmark's in-run ceilings) exports every call that
+    include/fkm_calib.h declares and rejects bad arguments on the host."""
+    path = os.path.join(ROOT, "paper_2608_12629_amd", "libfkm_calib.so")
+    if not os.path.exists(path):
+        pytest.fail(f"{path} not built (run __graft_entry__.build())")
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "fkm_calib.h")).read(),
+                  flags=re.S)
+    names = sorted(set(re.findall(r"\b(fkm_calib_\w+)\s*\(", text)))
+    assert names == ["fkm_calib_gather", "fkm_calib_mfma", "fkm_calib_read"]
+    L = ctypes.CDLL(path)
+    for n in names:
+        assert hasattr(L, n), n
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    L.fkm_calib_mfma.argtypes = [vp, i32, i32, vp]
+    L.fkm_calib_read.argtypes = [vp, sz, vp, i32, vp]
+    L.fkm_calib_gather.argtypes = [vp, i64, i32, vp, i64, vp, i32, vp]
+    assert L.fkm_calib_mfma(None, 512, 10, None) == -1
+    assert L.fkm_calib_mfma(FAKE, 0, 10, None) == -1
+    assert L.fkm_calib_read(FAKE, 17, FAKE, 16, None) == -1        # not whole 16-byte chunks
+    assert L.fkm_calib_read(FAKE + 4, 16, FAKE, 16, None) == -1    # misaligned
+    assert L.fkm_calib_gather(FAKE, 10, 2048, FAKE, 10, FAKE, 16, None) == -1  # rows > 1 KiB
+    assert L.fkm_calib_gather(FAKE, 0, 256, FAKE, 10, FAKE, 16, None) == -1
