@@ -50,6 +50,25 @@ namespace fkm {
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
+// One 16-byte-per-lane load from global memory straight into LDS (lane l
+// writes LDS byte lds + 16 l), issued as assembly: with the compiler's
+// builtin for it in flight, the compiler's own waits before every LDS read
+// became full drains (lgkmcnt(0), even vmcnt(0)), although no read here
+// touches the buffer being filled.  Outside its view the loads count only in
+// the hardware's in-order vmcnt; the stage ends wait for them explicitly
+// (s_waitcnt vmcnt(0) and a barrier) before any read of that buffer, and the
+// compiler's waits for its own loads stay correct because loads complete in
+// issue order.  M0 (the LDS base) is set here; nothing else in these kernels
+// uses it.
+__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
+  const uint32_t base =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(base)
+               : "memory");
+}
+
 // Per-lane offsets, fixed for the whole kernel.
 template <int CPL, int LOADS>
 struct PipeOffsets {
@@ -104,11 +123,27 @@ __device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat
   const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
-  for (int u = 0; u < LOADS; ++u)
-    __builtin_amdgcn_global_load_lds((global_void*)(src + o.src[u]),
-                                     (lds_void*)(buf + (u * ASSIGN_THREADS + wave * 64) * 16), 16, 0,
-                                     0);
+  for (int u = 0; u < LOADS; ++u) lds_dma16(src + o.src[u], buf + (u * ASSIGN_THREADS + wave * 64) * 16);
   return cinit[st * L::TCS + (tid & (L::TCS - 1))];
+}
+
+// Rows row0 .. row0 + TCS - 1 of X (rows past N - 1 repeat row N - 1) into
+// `buf` in the stage layout: the same slots, swizzle and per-lane offsets as
+// a centroid stage, so each load instruction of a wave fetches whole
+// consecutive rows (coalesced) and a lane's fragments are read back with the
+// stage's offsets.  Complete after the wave's next vmcnt(0) wait and a barrier.
+template <int CPL, int LOADS>
+__device__ __forceinline__ void pipe_issue_rows(const uint4* __restrict__ X, int row0, int N, int tid,
+                                                char* buf) {
+  using L = PipeLayout<CPL>;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) {
+    const int sl = tid + u * ASSIGN_THREADS;
+    const int r = sl / L::RCP, c = (sl % L::RCP) ^ (r & L::SWZ);
+    const int row = min(row0 + r, N - 1);
+    lds_dma16(X + (size_t)row * L::RC + (c < L::RC ? c : 0), buf + (u * ASSIGN_THREADS + wave * 64) * 16);
+  }
 }
 
 // The MFMAs of one 32-centroid tile into acc; each chain starts from the scores' init.
@@ -234,10 +269,39 @@ __device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
 
   PipeOffsets<CPL, LOADS> o;
   pipe_offsets<CPL, LOADS>(o, tid, n, h);
-  const float n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
-
   const int pbase = blk * PPB + wave * PPW;
   uint4 xr[NSUB][CPL];
+  // The block's points to registers.  When they fill exactly the two stage
+  // buffers, they go through LDS: loaded row-contiguous (each instruction
+  // fetches whole rows), then read in the matrix-operand layout.  A lane's
+  // direct fragments (16 bytes of each of 32 rows per instruction) cost about
+  // as long again from cache as from memory: the loads' own cost, not the
+  // latency.  The first centroid stage then follows into buf0.
+  constexpr bool XLDS = PPB == 2 * L::TCS;
+  float n0;
+  if constexpr (XLDS) {
+    pipe_issue_rows<CPL, LOADS>(X, blk * PPB, N, tid, buf0);
+    pipe_issue_rows<CPL, LOADS>(X, blk * PPB + L::TCS, N, tid, buf1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    char* xb = wave * PPW < L::TCS ? buf0 : buf1;   // the wave's rows (uniform)
+    const int t0 = (wave * PPW % L::TCS) / 32;       // its first 32-row tile there
+#pragma unroll
+    for (int p = 0; p < NSUB; ++p)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) xr[p][c] = lds_at<uint4>(xb, o.a[c], (t0 + p) * L::TILE);
+    __syncthreads();  // every wave has its rows before buf0 takes the first stage
+    n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
+  } else {
+    n0 = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
+#pragma unroll
+    for (int p = 0; p < NSUB; ++p) {
+      const int pt = pbase + p * 32 + n;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        xr[p][c] = pt < N ? X[(size_t)pt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
+    }
+  }
   float xn[NSUB];
   float xmax = 0.f, xmin = __builtin_inff();
 #pragma unroll
@@ -246,10 +310,7 @@ __device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
     const bool ok = pt < N;
     float ss = 0.f;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      xr[p][c] = ok ? X[(size_t)pt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
-      ss = chunk_sumsq<DT>(xr[p][c], ss);
-    }
+    for (int c = 0; c < CPL; ++c) ss = chunk_sumsq<DT>(xr[p][c], ss);
     ss += __shfl_xor(ss, 32);
     xn[p] = ss;
     xmax = __builtin_fmaxf(xmax, ss);
