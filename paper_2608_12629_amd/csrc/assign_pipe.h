@@ -432,9 +432,10 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_kernel(
 }
 
 // The flagged blocks, each point shifted by its own bound.  A fixed grid of
-// workgroups walks the blocks (block blockIdx.x, then every gridDim.x-th) and
-// skips the unflagged ones, so with no wide block it costs one read of the
-// flags.
+// workgroups splits the blocks into contiguous ranges; each wave reads 64
+// flags of its range at once (one per lane) and the workgroup assigns the
+// flagged blocks among them, so with no wide block it costs one read of the
+// flags per 64 blocks.
 template <int DT, int CPL, int NSUB>
 __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_wide_kernel(
     const uint4* __restrict__ X, const uint4* __restrict__ chat, const float* __restrict__ cinit,
@@ -446,14 +447,22 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_pipe_wide_kernel(
   __shared__ double lds_obj[4];
   const int b = blockIdx.y;
   const int32_t* wb = wide + (size_t)b * nblk;
-  for (int blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
-    if (wb[blk] == 0) continue;  // one address for the whole workgroup: uniform
-    pipe_block<DT, CPL, NSUB, true>(
-        blk, X + (size_t)b * N * L::RC,
-        reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * L::RC, cinit + (size_t)b * Kp, N,
-        Kp / L::TCS, idx + (size_t)b * N, min_dist + (size_t)b * N, objpart + (size_t)b * nblk,
-        nullptr, buf0, buf1, nullptr, nullptr, lds_obj);
-    __syncthreads();  // every wave is done with the stage buffers before the next block
+  const int per = (nblk + gridDim.x - 1) / gridDim.x;
+  const int r0 = blockIdx.x * per, r1 = min(r0 + per, nblk);
+  for (int g0 = r0; g0 < r1; g0 += 64) {
+    const int bl = g0 + (threadIdx.x & 63);
+    // every wave reads the same 64 flags, so the mask is the same in all of them
+    uint64_t m = __ballot(bl < r1 && wb[bl] != 0);
+    while (m != 0) {
+      const int blk = g0 + __builtin_ctzll(m);
+      m &= m - 1;
+      pipe_block<DT, CPL, NSUB, true>(
+          blk, X + (size_t)b * N * L::RC,
+          reinterpret_cast<const u32x4*>(chat) + (size_t)b * Kp * L::RC, cinit + (size_t)b * Kp, N,
+          Kp / L::TCS, idx + (size_t)b * N, min_dist + (size_t)b * N, objpart + (size_t)b * nblk,
+          nullptr, buf0, buf1, nullptr, nullptr, lds_obj);
+      __syncthreads();  // every wave is done with the stage buffers before the next block
+    }
   }
 }
 

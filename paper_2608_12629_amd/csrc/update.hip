@@ -68,7 +68,11 @@ __device__ __forceinline__ int block_scan256(int v, int* wsum, int& total) {
 // start) into chunks of at most RADIX_CHUNK entries, ceil(T1[r] / RADIX_CHUNK)
 // of them, numbered bin by bin, so every chunk holds a single low digit.
 // Chunk `ch` of instance b: entries [e0, e1) with low digit `lo` (an empty
-// range past the last chunk).  Called by all 256 threads; wsum: 8 ints.
+// range past the last chunk).  sel[3..4] get the low digits whose first chunk
+// (cq, the chunks before the digit's) is `ch`: the digit of a chunk that
+// starts one and the empty digits just before it, or past the last chunk the
+// empty digits at the end (an empty range: sel[3] > sel[4] otherwise).
+// Called by all 256 threads; wsum: 8 ints, sel: 5.
 __device__ inline void lo_chunk(const int32_t* __restrict__ T1, int b, int R1, int ch, int* wsum,
                                 int* sel, int& e0, int& e1, int& lo) {
   const int t = threadIdx.x;
@@ -77,13 +81,21 @@ __device__ inline void lo_chunk(const int32_t* __restrict__ T1, int b, int R1, i
   int all;
   const int start = block_scan256(cnt, wsum, all);
   const int cq = block_scan256(q, wsum + 4, all);
-  if (t == 0) sel[0] = sel[1] = sel[2] = 0;
+  if (t == 0) {
+    sel[0] = sel[1] = sel[2] = 0;
+    sel[3] = R1;
+    sel[4] = -1;
+  }
   __syncthreads();
   if (q > 0 && cq <= ch && ch < cq + q) {  // one thread at most
     const int a = start + (ch - cq) * RADIX_CHUNK;
     sel[0] = a;
     sel[1] = min(a + RADIX_CHUNK, start + cnt);
     sel[2] = t;
+  }
+  if (t < R1 && cq == ch) {  // cq is non-decreasing in t: a run of threads
+    atomicMin(&sel[3], t);
+    atomicMax(&sel[4], t);
   }
   __syncthreads();
   e0 = sel[0];
@@ -102,7 +114,7 @@ __global__ __launch_bounds__(256) void radix_hist_kernel(const int32_t* __restri
                                                          const int32_t* __restrict__ T1,
                                                          int lo_bits) {
   __shared__ int cnt[RADIX_MAX_R];
-  __shared__ int wsum[8], sel[3];
+  __shared__ int wsum[8], sel[5];
   const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
   int e0, e1, lo;
   if (pb) {
@@ -171,19 +183,35 @@ __global__ __launch_bounds__(256) void radix_scan_kernel(int32_t* __restrict__ H
 //   (key >> lo_bits) << pb | point id.
 // MODE 2 (second pass, packed): packed words in, in the chunks of lo_chunk,
 //   so a chunk's low digit is known and restores each key; point ids out.
+//
+// Ranking.  Each wave takes a quarter of the chunk in entry order, in steps
+// of 64 entries.  In a step the lanes holding one digit find each other with
+// one ballot per digit bit; the lowest of them adds the group's size to the
+// wave's count of that digit with an LDS atomic that returns the count before
+// it, and the others read that from it.  A wave's atomics execute in program
+// order, so these counts are exact and the same on every run; all its steps'
+// atomics are issued back to back and waited for once.  After a scan over
+// digits and waves, an entry's place in the chunk sorted by digit is the start
+// of its digit + its wave's start within the digit + the count before its
+// step + its rank among its step's lanes of that digit.  The chunk is staged
+// there in LDS (the output word and the digit, one byte) and written out in
+// sorted order, so each digit's run goes out contiguously (coalesced).
 template <int DBITS, int MODE>
 __global__ __launch_bounds__(256) void radix_scatter_kernel(
     const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int N, int K,
     const int32_t* __restrict__ total, int shift, int nch,
     const int32_t* __restrict__ H, const int32_t* __restrict__ T, int32_t* __restrict__ total_out,
     int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out, int lo_bits, int pb,
-    const int32_t* __restrict__ T1) {
+    const int32_t* __restrict__ T1, int32_t* __restrict__ off) {
   constexpr int STEPS = RADIX_CHUNK / 256;  // 64-entry steps per wave
-  __shared__ int skey[RADIX_CHUNK], sval[RADIX_CHUNK];
-  __shared__ int cur[4][RADIX_MAX_R];
-  __shared__ int lstart[RADIX_MAX_R], gstart[RADIX_MAX_R];
-  __shared__ int wsum[4][4], sel[3];
   constexpr int R = 1 << DBITS;
+  static_assert(R <= 256, "one thread per digit in the scans");
+  __shared__ int sval[RADIX_CHUNK];                 // output words in sorted order
+  __shared__ int skey[MODE == 0 ? RADIX_CHUNK : 1];  // keys too when they are written out
+  __shared__ uint8_t sdg[RADIX_CHUNK];              // digit of each sorted entry
+  __shared__ int cnt[4][R];                          // per-wave digit counts, then starts
+  __shared__ int gdelta[R];
+  __shared__ int wsum[4][4], sel[5];
   const int b = blockIdx.y, ch = blockIdx.x, t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   int e0, e1, lo_c = 0;
@@ -198,80 +226,128 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   const int32_t* vb = vals_in ? vals_in + (size_t)b * N : nullptr;
   const int ibase = e0 + w * (RADIX_CHUNK / 4);
 
-  int k[STEPS], v[STEPS];
+  // the input word of each entry; the packed modes rebuild key and output
+  // word from it (and the entry index) when needed, so only MODE 0 keeps a
+  // value per entry
+  int k[STEPS], v[MODE == 0 ? STEPS : 1];
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
     const int i = ibase + s * 64 + lane;
     const bool in = i < e1;
     k[s] = in ? kb[i] : -1;
-    v[s] = in ? (vb ? vb[i] : i) : 0;
+    if constexpr (MODE == 0) v[s] = in ? (vb ? vb[i] : i) : 0;
   }
   // this bin's total over all chunks and its count before this chunk
   const int tbin = t < R ? T[(size_t)b * RADIX_MAX_R + t] : 0;
   const int hrun = t < R ? H[((size_t)b * R + t) * nch + ch] : 0;
+  if (t < R) {
 #pragma unroll
-  for (int ww = 0; ww < 4; ++ww) cur[ww][t] = 0;  // RADIX_MAX_R == 256 == blockDim
+    for (int ww = 0; ww < 4; ++ww) cnt[ww][t] = 0;
+  }
   // bin starts: exclusive scan of the bin totals (its barrier also orders the zeroing)
   int n_valid;
   const int bstart = block_scan256(tbin, wsum[0], n_valid);
   if (total_out && ch == 0 && t == 0) total_out[b] = n_valid;
-  if constexpr (MODE == 2) {  // key = high digit (packed) above the chunk's low digit
-    const int pmask = (int)((1u << pb) - 1u);
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      if (k[s] >= 0) {
-        v[s] = k[s] & pmask;
-        k[s] = ((k[s] >> pb) << lo_bits) | lo_c;
+  const int pmask = (int)((1u << pb) - 1u);
+  if constexpr (MODE == 2) {
+    // Cluster offsets: key (hi, lo) starts where digit hi's entries of the
+    // first chunk of low digit lo go (bin start + the count before that
+    // chunk); low digits with no entries share the next chunk's, those past
+    // the last one the chunk past the end (always in the grid).  The chunk
+    // of those low digits writes them, one thread per high digit.
+    if (t < R) {
+      const int a = min(max(bstart + hrun, 0), n_valid);
+      int32_t* ob = off + (size_t)b * (K + 1);
+      for (int l = sel[3]; l <= sel[4]; ++l) {
+        const int key = (t << lo_bits) | l;
+        if (key < K) ob[key] = a;
       }
+      if (ch == 0 && t == 0) ob[K] = n_valid;
     }
   }
-  // per-wave bin counts (integer atomics: exact)
+  // rank in entry order within each wave (see above)
+  const uint32_t blo = lane >= 32 ? ~0u : (1u << lane) - 1u;  // lanes below this one
+  const uint32_t bhi = lane <= 32 ? 0u : ~0u >> (64 - lane);
+  // per step: digit (bits 0-7), rank (8-13), the digit group's lowest lane
+  // (16-21), 1 << 24 for an entry (every digit value of 8-bit digits is a real
+  // digit); and the count before the step
+  int meta[STEPS], old[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+    int key;
+    if constexpr (MODE == 2)  // high digit above the chunk's low digit
+      key = k[s] >= 0 ? ((k[s] >> pb) << lo_bits) | lo_c : -1;
+    else
+      key = k[s];
+    const bool valid = (unsigned)key < (unsigned)K;
+    const int dg = valid ? digit_of(key, shift, R) : 0;
+    // lanes holding the same digit: for each bit keep the lanes that agree,
+    // on the two 32-lane halves (invalid lanes hold digit 0 and are dropped
+    // by the first ballot)
+    const uint64_t vm = __ballot(valid);
+    uint32_t mlo = (uint32_t)vm, mhi = (uint32_t)(vm >> 32);
+#pragma unroll
+    for (int bit = 0; bit < DBITS; ++bit) {
+      const int m = (int)((uint32_t)dg << (31 - bit)) >> 31;  // all ones where the bit is set
+      const uint64_t bb = __ballot(m != 0);
+      mlo &= ~((uint32_t)bb ^ (uint32_t)m);
+      mhi &= ~((uint32_t)(bb >> 32) ^ (uint32_t)m);
+    }
+    const int rank = __popc(mlo & blo) + __popc(mhi & bhi);
+    const int lead = !valid ? lane : mlo ? __builtin_ctz(mlo) : 32 + __builtin_ctz(mhi);
+    int ms = dg | (rank << 8) | (lead << 16) | (valid ? 1 << 24 : 0);
+    // one register per step from here on: the fields are read back from it,
+    // not kept apart (which took four per step)
+    asm volatile("" : "+v"(ms));
+    meta[s] = ms;
+    int before = 0;  // a scalar across the branch (an array there is copied whole)
+    if (valid && rank == 0) before = atomicAdd(&cnt[w][dg], __popc(mlo) + __popc(mhi));
+    old[s] = before;
+    // one step at a time: hoisting every step's ballots ahead of the atomics
+    // took all 256 registers
+    __builtin_amdgcn_sched_barrier(0);
+  }
 #pragma unroll
   for (int s = 0; s < STEPS; ++s)
-    if ((unsigned)k[s] < (unsigned)K) atomicAdd(&cur[w][digit_of(k[s], shift, R)], 1);
+    old[s] = __shfl(old[s], (meta[s] >> 16) & 63) + ((meta[s] >> 8) & 63);
   __syncthreads();
   // this chunk's count per bin -> exclusive scan over bins; wave starts per bin
   int c4[4], tot = 0;
 #pragma unroll
   for (int ww = 0; ww < 4; ++ww) {
-    c4[ww] = t < R ? cur[ww][t] : 0;
+    c4[ww] = t < R ? cnt[ww][t] : 0;
     tot += c4[ww];
   }
   int nloc;
   const int ls = block_scan256(tot, wsum[1], nloc);
   if (t < R) {
-    lstart[t] = ls;
-    gstart[t] = bstart + hrun;
+    gdelta[t] = bstart + hrun - ls;  // output position = gdelta[digit] + sorted position
     int run = ls;
 #pragma unroll
     for (int ww = 0; ww < 4; ++ww) {
-      cur[ww][t] = run;
+      cnt[ww][t] = run;
       run += c4[ww];
     }
   }
   __syncthreads();
-  // rank in entry order within each wave and stage the chunk sorted by bin
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // stage the chunk sorted by digit, with its output words
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    const bool valid = (unsigned)k[s] < (unsigned)K;
-    const int dg = valid ? digit_of(k[s], shift, R) : 0;
-    // lanes holding the same digit: for each bit keep the lanes that agree
-    // (invalid lanes hold digit 0 and are dropped by the first ballot)
-    uint64_t match = __ballot(valid);
-#pragma unroll
-    for (int bit = 0; bit < DBITS; ++bit) {
-      const int on = (dg >> bit) & 1;
-      const uint64_t bb = __ballot(on);
-      const uint64_t flip = (uint64_t)(int64_t)(on - 1);  // all ones where the bit is clear
-      match &= bb ^ flip;
-    }
-    if (valid) {
-      const int rank = __popcll(match & below);
-      const int start = cur[w][dg];
-      if (rank == 0) cur[w][dg] = start + __popcll(match);
-      skey[start + rank] = k[s];
-      sval[start + rank] = v[s];
+    const int ms = meta[s];
+    const int dg = ms & 255;
+    if (ms & (1 << 24)) {
+      const int pos = cnt[w][dg] + old[s];
+      int out;
+      if constexpr (MODE == 0) {
+        out = v[s];
+        skey[pos] = k[s];
+      } else if constexpr (MODE == 1) {  // high digit above the point id
+        out = ((k[s] >> lo_bits) << pb) | (ibase + s * 64 + lane);
+      } else {  // the point id
+        out = k[s] & pmask;
+      }
+      sval[pos] = out;
+      sdg[pos] = (uint8_t)dg;
     }
   }
   __syncthreads();
@@ -282,63 +358,19 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   for (int s = 0; s < STEPS; ++s) {
     const int j = s * 256 + t;
     if (j < nloc) {
-      const int key = skey[j];
-      const int dg = digit_of(key, shift, R);
-      const int g = gstart[dg] + (j - lstart[dg]);
-      if (ko) ko[g] = key;
-      vo[g] = MODE == 1 ? (((key >> lo_bits) << pb) | sval[j]) : sval[j];
+      const int g = gdelta[sdg[j] & (R - 1)] + j;
+      vo[g] = sval[j];
+      if constexpr (MODE == 0)
+        if (ko) ko[g] = skey[j];
     }
   }
 }
 
-// Cluster offsets and counts after the packed passes (no sorted keys, no
-// atomics): for key k = (hi, lo), off[k] = the entries of lower high digits
-// plus those of digit hi in the chunks before lo's first chunk (the second
-// pass's scanned histogram at that chunk; all of digit hi past the last
-// chunk); count_k = off[k+1] - off[k], off[K] = the valid total.  One key per
-// thread; offsets are capped to [0, total].
-__global__ __launch_bounds__(256) void offsets_kernel(const int32_t* __restrict__ Hs,
-                                                      const int32_t* __restrict__ T2,
-                                                      const int32_t* __restrict__ T1,
-                                                      const int32_t* __restrict__ total, int K,
-                                                      int lo_bits, int R2, int nch2,
-                                                      int32_t* __restrict__ off,
-                                                      int32_t* __restrict__ counts) {
-  __shared__ int wsum[2][4];
-  __shared__ int cq_s[RADIX_MAX_R], bs_s[RADIX_MAX_R], t2_s[RADIX_MAX_R], off_s[256];
-  const int b = blockIdx.y, t = threadIdx.x;
-  const int k = blockIdx.x * 256 + t;  // 0 .. K
-  const int R1 = 1 << lo_bits;
-  const int c1 = t < R1 ? T1[(size_t)b * RADIX_MAX_R + t] : 0;
-  int all;
-  cq_s[t] = block_scan256((c1 + RADIX_CHUNK - 1) / RADIX_CHUNK, wsum[0], all);
-  const int t2 = t < R2 ? T2[(size_t)b * RADIX_MAX_R + t] : 0;
-  t2_s[t] = t2;
-  bs_s[t] = block_scan256(t2, wsum[1], all);
-  __syncthreads();
-  const int nv = total[b];
-  const int32_t* hb = Hs + (size_t)b * R2 * nch2;
-  auto at = [&](int kk) -> int {
-    if (kk >= K) return nv;
-    const int hi = kk >> lo_bits, c = cq_s[kk & (R1 - 1)];
-    const int before = c < nch2 ? hb[(size_t)hi * nch2 + c] : t2_s[hi];
-    return min(max(bs_s[hi] + before, 0), nv);
-  };
-  const int a = k <= K ? at(k) : 0;
-  off_s[t] = a;
-  __syncthreads();
-  if (k <= K) {
-    off[(size_t)b * (K + 1) + k] = a;
-    if (k < K) counts[(size_t)b * K + k] = (t < 255 ? off_s[t + 1] : at(k + 1)) - a;
-  }
-}
-
-// Cluster offsets and counts from the sorted keys: off[k] = first position of
-// a key >= k (binary search), count_k = off[k+1] - off[k].
+// Cluster offsets from the sorted keys: off[k] = first position of a key >= k
+// (binary search); the counts are off[k+1] - off[k].
 __global__ __launch_bounds__(256) void bounds_kernel(const int32_t* __restrict__ sorted,
                                                      const int32_t* __restrict__ total, int N, int K,
-                                                     int32_t* __restrict__ off,
-                                                     int32_t* __restrict__ counts) {
+                                                     int32_t* __restrict__ off) {
   const int k = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
   if (k > K) return;
   const int n = total[b];
@@ -351,9 +383,7 @@ __global__ __launch_bounds__(256) void bounds_kernel(const int32_t* __restrict__
     }
     return lo;
   };
-  const int a = lower(k);
-  off[(size_t)b * (K + 1) + k] = a;
-  if (k < K) counts[(size_t)b * K + k] = lower(k + 1) - a;
+  off[(size_t)b * (K + 1) + k] = lower(k);
 }
 
 // ---------------------------------------------------------------------------
@@ -541,11 +571,12 @@ __device__ inline float4 f4div(float4 s, float n) {
   return make_float4(s.x / n, s.y / n, s.z / n, s.w / n);
 }
 
-// Per cluster, the sum (one slice, or the slices' carries in slice order)
-// over the count; an empty cluster keeps its previous centroid.
+// Per cluster, the count (the length of its run in the sorted order, written
+// out) and the sum (one slice, or the slices' carries in slice order) over
+// the count; an empty cluster keeps its previous centroid.
 __global__ __launch_bounds__(256) void finalize_kernel(
     const float* __restrict__ sums, const float* __restrict__ carry,
-    const int32_t* __restrict__ counts, const int32_t* __restrict__ off,
+    int32_t* __restrict__ counts, const int32_t* __restrict__ off,
     const float* C_prev, int K, int D, int nred, int cr, float* C_out, NextStep nx) {
   __shared__ float4 part[256];
   extern __shared__ float4 row4_dyn[];  // the groups' new centroid rows (D floats each)
@@ -560,9 +591,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(
   const size_t rowoff = ((size_t)b * K + k) * D;
   int n = 0, j0 = 0, c0 = 0, c1 = 0;
   if (valid) {
-    n = counts[(size_t)b * K + k];
     j0 = off[(size_t)b * (K + 1) + k];
     const int j1 = off[(size_t)b * (K + 1) + k + 1];
+    n = j1 - j0;
+    if (t % TPC == 0) counts[(size_t)b * K + k] = n;
     c0 = j0 / cr;
     c1 = n == 0 ? c0 : (j1 - 1) / cr;
   }
@@ -988,7 +1020,7 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
     if ((e = launch_scatter<1>(d1, cgrid, s, idx, (const int32_t*)nullptr, (int)N, (int)K,
                                (const int32_t*)nullptr, 0, nch, (const int32_t*)w.rhist,
                                (const int32_t*)w.rbin1, w.rtotal, (int32_t*)nullptr, w.keys_a, d1,
-                               pb, (const int32_t*)nullptr)) != hipSuccess)
+                               pb, (const int32_t*)nullptr, (int32_t*)nullptr)) != hipSuccess)
       return e;
     const dim3 cgrid2(nch2, (unsigned)B);
     radix_hist_kernel<<<cgrid2, 256, 0, s>>>(w.keys_a, (int)N, (int)K, nullptr, 0, R2, nch2,
@@ -1000,11 +1032,8 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
                                (int)N, (int)K, (const int32_t*)nullptr, d1, nch2,
                                (const int32_t*)w.rhist, (const int32_t*)w.rbin, (int32_t*)nullptr,
                                (int32_t*)nullptr, w.perm, d1, pb,
-                               (const int32_t*)w.rbin1)) != hipSuccess)
+                               (const int32_t*)w.rbin1, w.off)) != hipSuccess)
       return e;
-    offsets_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
-        w.rhist, w.rbin, w.rbin1, w.rtotal, (int)K, d1, R2, nch2, w.off, counts);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
     // pass 1: idx (raw) -> (keys_a, vals_a) sorted by the low digit; with one
     // pass the values go straight to perm and the keys to keys_b
@@ -1018,7 +1047,7 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
                                (const int32_t*)nullptr, 0, nch, (const int32_t*)w.rhist,
                                (const int32_t*)w.rbin, w.rtotal,
                                passes == 1 ? w.keys_b : w.keys_a, passes == 1 ? w.perm : w.vals_a,
-                               0, 0, (const int32_t*)nullptr)) != hipSuccess)
+                               0, 0, (const int32_t*)nullptr, (int32_t*)nullptr)) != hipSuccess)
       return e;
     if (passes == 2) {
       const int R2 = 1 << d2;
@@ -1030,12 +1059,12 @@ hipError_t launch_update(const void* X, int dt, const int32_t* idx, const float*
       if ((e = launch_scatter<0>(d2, cgrid, s, (const int32_t*)w.keys_a, (const int32_t*)w.vals_a,
                                  (int)N, (int)K, (const int32_t*)w.rtotal, d1, nch,
                                  (const int32_t*)w.rhist, (const int32_t*)w.rbin, (int32_t*)nullptr,
-                                 w.keys_b, w.perm, 0, 0,
-                                 (const int32_t*)nullptr)) != hipSuccess)  // the same total
+                                 w.keys_b, w.perm, 0, 0, (const int32_t*)nullptr,
+                                 (int32_t*)nullptr)) != hipSuccess)  // the same total
         return e;
     }
     bounds_kernel<<<dim3((unsigned)((K + 1 + 255) / 256), (unsigned)B), 256, 0, s>>>(
-        w.keys_b, w.rtotal, (int)N, (int)K, w.off, counts);
+        w.keys_b, w.rtotal, (int)N, (int)K, w.off);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (dt == DT_BF16) e = launch_segreduce_dt<DT_BF16>(X, w, B, N, D, K, s);
