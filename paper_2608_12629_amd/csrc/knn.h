@@ -90,22 +90,29 @@ __device__ __forceinline__ void knn_insert_by_index(float (&v)[KMAX], int (&ix)[
   }
 }
 
-// The MFMAs of one 32-row tile (tile index at run time) into acc.
-template <int DT, int CPL, int LOADS>
-__device__ __forceinline__ void knn_mfma_tile(f32x16& acc, const uint4 (&xr)[1][CPL], char* buf,
-                                              const PipeOffsets<CPL, LOADS>& o, int tile) {
+// The MFMAs of one 32-row tile (tile index at run time) into acc, one
+// accumulator per 32-query tile: each row fragment read from LDS feeds NSUB
+// MFMAs, and the scores are read once for all of them.
+template <int DT, int CPL, int NSUB, int LOADS>
+__device__ __forceinline__ void knn_mfma_tile(f32x16 (&acc)[NSUB], const uint4 (&xr)[NSUB][CPL],
+                                              char* buf, const PipeOffsets<CPL, LOADS>& o,
+                                              int tile) {
   using L = PipeLayout<CPL>;
+  f32x16 cin;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const f32x4 v = lds_at<f32x4>(buf, o.n_read + (tile * 32 + 8 * q) * 4, 0);
-    acc[4 * q + 0] = v[0];
-    acc[4 * q + 1] = v[1];
-    acc[4 * q + 2] = v[2];
-    acc[4 * q + 3] = v[3];
+    cin[4 * q + 0] = v[0];
+    cin[4 * q + 1] = v[1];
+    cin[4 * q + 2] = v[2];
+    cin[4 * q + 3] = v[3];
   }
 #pragma unroll
-  for (int c = 0; c < CPL; ++c)
-    acc = mfma32_chunk<DT>(lds_at<uint4>(buf, o.a[c] + tile * L::TILE, 0), xr[0][c], acc);
+  for (int c = 0; c < CPL; ++c) {
+    const uint4 a = lds_at<uint4>(buf, o.a[c] + tile * L::TILE, 0);
+#pragma unroll
+    for (int p = 0; p < NSUB; ++p) acc[p] = mfma32_chunk<DT>(a, xr[p][c], c == 0 ? cin : acc[p]);
+  }
 }
 
 // Score j of the tile (a select chain: j differs per lane).
@@ -154,31 +161,34 @@ __device__ __forceinline__ void knn_update(const f32x16& acc, int base, float (&
 // accumulator sets: the matrix pipe and the vector ALU overlap only within a
 // wave's own instruction stream).  Store the next stage's scores, wait for
 // its loads and sync.
-template <int DT, int CPL, int KMAX, int LOADS>
+template <int DT, int CPL, int NSUB, int KMAX, int LOADS>
 __device__ __forceinline__ void knn_stage(int st, int nst, char* cur, char* nxt,
                                           const PipeOffsets<CPL, LOADS>& o,
-                                          const uint4 (&xr)[1][CPL], const u32x4* chat4,
-                                          const float* cinit, int tid, int h, float (&v)[KMAX],
-                                          int (&ix)[KMAX]) {
+                                          const uint4 (&xr)[NSUB][CPL], const u32x4* chat4,
+                                          const float* cinit, int tid, int h,
+                                          float (&v)[NSUB][KMAX], int (&ix)[NSUB][KMAX]) {
   using L = PipeLayout<CPL>;
   const bool more = st + 1 < nst;
   float nn = 0.f;
   if (more) nn = pipe_issue_stage<CPL, LOADS>(chat4, cinit, st + 1, tid, o, nxt);
   if constexpr (KMAX > 16) {
-    f32x16 acc[2];
-    knn_mfma_tile<DT, CPL, LOADS>(acc[0], xr, cur, o, 0);
+    static_assert(NSUB == 1, "32-entry lists keep one query tile per wave");
+    f32x16 acc[2][1];
+    knn_mfma_tile<DT, CPL, 1, LOADS>(acc[0], xr, cur, o, 0);
 #pragma unroll
     for (int tile = 0; tile < L::TILES; ++tile) {
       if (tile + 1 < L::TILES)
-        knn_mfma_tile<DT, CPL, LOADS>(acc[(tile + 1) & 1], xr, cur, o, tile + 1);
-      knn_update<KMAX>(acc[tile & 1], (st * L::TILES + tile) * 32 + 4 * h, v, ix);
+        knn_mfma_tile<DT, CPL, 1, LOADS>(acc[(tile + 1) & 1], xr, cur, o, tile + 1);
+      knn_update<KMAX>(acc[tile & 1][0], (st * L::TILES + tile) * 32 + 4 * h, v[0], ix[0]);
     }
   } else {
     // within 256 registers the second accumulator set costs spills
     for (int tile = 0; tile < L::TILES; ++tile) {
-      f32x16 acc;
-      knn_mfma_tile<DT, CPL, LOADS>(acc, xr, cur, o, tile);
-      knn_update<KMAX>(acc, (st * L::TILES + tile) * 32 + 4 * h, v, ix);
+      f32x16 acc[NSUB];
+      knn_mfma_tile<DT, CPL, NSUB, LOADS>(acc, xr, cur, o, tile);
+#pragma unroll
+      for (int p = 0; p < NSUB; ++p)
+        knn_update<KMAX>(acc[p], (st * L::TILES + tile) * 32 + 4 * h, v[p], ix[p]);
     }
   }
   if (more) lds_at<float>(nxt, o.n_store, 0) = nn;
@@ -188,7 +198,10 @@ __device__ __forceinline__ void knn_stage(int st, int nst, char* cur, char* nxt,
 
 // Lists of 8 or 16 fit two waves per SIMD (the update's latency then hides
 // behind the other wave's MFMAs); 32 entries take the whole register file.
-template <int DT, int CPL, int KMAX>
+// NSUB 32-query tiles per wave: with two, each row fragment read from LDS
+// feeds two MFMAs (with one, the four SIMDs' fragment and score reads ask
+// more of the LDS than the matrix pipes take in).
+template <int DT, int CPL, int NSUB, int KMAX>
 __global__ __launch_bounds__(ASSIGN_THREADS, KMAX <= 16 ? 2 : 1) void knn_kernel(
     const uint4* __restrict__ Q, const uint4* __restrict__ chat, const float* __restrict__ cinit,
     int M, int Np, int k, int32_t* __restrict__ nbr_idx, float* __restrict__ nbr_dist) {
@@ -196,7 +209,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS, KMAX <= 16 ? 2 : 1) void knn_kernel
   constexpr int RC = L::RC;
   constexpr int LOADS = L::TCS * L::RCP / ASSIGN_THREADS;
   static_assert(LOADS >= 1 && LOADS * ASSIGN_THREADS == L::TCS * L::RCP, "stage must split evenly");
-  constexpr int QPB = 4 * 32;  // queries per workgroup
+  constexpr int QPW = 32 * NSUB, QPB = 4 * QPW;  // queries per wave, per workgroup
 
   __shared__ __attribute__((aligned(16))) char buf0[L::STAGE];
   __shared__ __attribute__((aligned(16))) char buf1[L::STAGE];
@@ -214,62 +227,82 @@ __global__ __launch_bounds__(ASSIGN_THREADS, KMAX <= 16 ? 2 : 1) void knn_kernel
   pipe_offsets<CPL, LOADS>(o, tid, n, h);
   float nn = pipe_issue_stage<CPL, LOADS>(chat4, cinit, 0, tid, o, buf0);
 
-  const int qt = blockIdx.x * QPB + wave * 32 + n;  // this lane's query
-  const bool qok = qt < M;
-  uint4 xr[1][CPL];
-  float ss = 0.f;
+  const int q0 = blockIdx.x * QPB + wave * QPW + n;  // this lane's query of tile 0
+  uint4 xr[NSUB][CPL];
+  float ss[NSUB];
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    xr[0][c] = qok ? Q[(size_t)qt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
-    ss = chunk_sumsq<DT>(xr[0][c], ss);
+  for (int p = 0; p < NSUB; ++p) {
+    const int qt = q0 + 32 * p;
+    float a = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      xr[p][c] = qt < M ? Q[(size_t)qt * RC + h * CPL + c] : make_uint4(0, 0, 0, 0);
+      a = chunk_sumsq<DT>(xr[p][c], a);
+    }
+    ss[p] = a + __shfl_xor(a, 32);
   }
-  ss += __shfl_xor(ss, 32);
 
-  float v[KMAX];
-  int ix[KMAX];
+  float v[NSUB][KMAX];
+  int ix[NSUB][KMAX];
 #pragma unroll
-  for (int t = 0; t < KMAX; ++t) {
-    v[t] = -__builtin_inff();
-    ix[t] = 0x7fffffff;
-  }
+  for (int p = 0; p < NSUB; ++p)
+#pragma unroll
+    for (int t = 0; t < KMAX; ++t) {
+      v[p][t] = -__builtin_inff();
+      ix[p][t] = 0x7fffffff;
+    }
 
   lds_at<float>(buf0, o.n_store, 0) = nn;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int st = 0;
   for (; st + 2 <= nst; st += 2) {  // two stages per trip: each buffer is a fixed array
-    knn_stage<DT, CPL, KMAX, LOADS>(st, nst, buf0, buf1, o, xr, chat4, cinit, tid, h, v, ix);
-    knn_stage<DT, CPL, KMAX, LOADS>(st + 1, nst, buf1, buf0, o, xr, chat4, cinit, tid, h, v, ix);
+    knn_stage<DT, CPL, NSUB, KMAX, LOADS>(st, nst, buf0, buf1, o, xr, chat4, cinit, tid, h, v, ix);
+    knn_stage<DT, CPL, NSUB, KMAX, LOADS>(st + 1, nst, buf1, buf0, o, xr, chat4, cinit, tid, h, v,
+                                          ix);
   }
-  if (st < nst) knn_stage<DT, CPL, KMAX, LOADS>(st, nst, buf0, buf1, o, xr, chat4, cinit, tid, h, v, ix);
+  if (st < nst)
+    knn_stage<DT, CPL, NSUB, KMAX, LOADS>(st, nst, buf0, buf1, o, xr, chat4, cinit, tid, h, v, ix);
 
-  // merge the other half's list (rows 4..7 of each group of 8) into lane h = 0's
 #pragma unroll
-  for (int t = 0; t < KMAX; ++t) {
-    const float so = __shfl_xor(v[t], 32);
-    const int io = __shfl_xor(ix[t], 32);
-    if (h == 0) knn_insert_by_index<KMAX>(v, ix, so, io);
-  }
-  if (h == 0 && qok) {
-    int32_t* oi = nbr_idx + ((size_t)b * M + qt) * k;
-    float* od = nbr_dist + ((size_t)b * M + qt) * k;
+  for (int p = 0; p < NSUB; ++p) {
+    // merge the other half's list (rows 4..7 of each group of 8) into lane h = 0's
 #pragma unroll
     for (int t = 0; t < KMAX; ++t) {
-      if (t < k) {
-        oi[t] = ix[t];
-        od[t] = __builtin_fmaxf(__builtin_fmaf(-2.f, v[t], ss), 0.f);
+      const float so = __shfl_xor(v[p][t], 32);
+      const int io = __shfl_xor(ix[p][t], 32);
+      if (h == 0) knn_insert_by_index<KMAX>(v[p], ix[p], so, io);
+    }
+    const int qt = q0 + 32 * p;
+    if (h == 0 && qt < M) {
+      int32_t* oi = nbr_idx + ((size_t)b * M + qt) * k;
+      float* od = nbr_dist + ((size_t)b * M + qt) * k;
+#pragma unroll
+      for (int t = 0; t < KMAX; ++t) {
+        if (t < k) {
+          oi[t] = ix[p][t];
+          od[t] = __builtin_fmaxf(__builtin_fmaf(-2.f, v[p][t], ss[p]), 0.f);
+        }
       }
     }
   }
 }
 
+// Two query tiles per wave where the lists leave room for them (16 entries
+// and D <= 128, which keeps two waves per SIMD), else one.
+template <int CPL, int KMAX>
+constexpr int knn_nsub() { return KMAX <= 16 && CPL <= 8 ? 2 : 1; }
+
 template <int DT, int CPL, int KMAX>
 hipError_t launch_knn_cpl(const void* Q, const void* chat, const float* cinit, int64_t B,
                           int64_t M, int64_t Np, int k, int32_t* nbr_idx, float* nbr_dist,
                           hipStream_t s) {
-  const dim3 grid((unsigned)((M + 127) / 128), (unsigned)B), block(ASSIGN_THREADS);
-  knn_kernel<DT, CPL, KMAX><<<grid, block, 0, s>>>((const uint4*)Q, (const uint4*)chat, cinit,
-                                                   (int)M, (int)Np, k, nbr_idx, nbr_dist);
+  constexpr int NSUB = knn_nsub<CPL, KMAX>();
+  constexpr int QPB = 4 * 32 * NSUB;
+  const dim3 grid((unsigned)((M + QPB - 1) / QPB), (unsigned)B), block(ASSIGN_THREADS);
+  knn_kernel<DT, CPL, NSUB, KMAX><<<grid, block, 0, s>>>((const uint4*)Q, (const uint4*)chat,
+                                                         cinit, (int)M, (int)Np, k, nbr_idx,
+                                                         nbr_dist);
   return hipGetLastError();
 }
 
