@@ -22,11 +22,18 @@
  *   at most 16 elements run as fp32 on exactly widened copies of the points
  *   (made in the workspace), so there the distances are to the fp32
  *   centroids themselves.
- * - Indices are int32 and local to an instance: idx[b, i] is in [0, K).
- * - Points and centroids must be finite.  (Non-finite values give unspecified
- *   results; with small K the sums are formed by multiplying every point by a
- *   0/1 membership, so one infinite coordinate turns that dimension of every
- *   cluster's mean into NaN.)
+ * - Indices are int32 and local to an instance: idx[b, i] is in [0, K), or -1
+ *   for a point left unassigned (below).
+ * - Non-finite values.  A point whose squared norm (accumulated in fp32) is
+ *   not finite -- a NaN or infinite coordinate -- is left unassigned: idx -1,
+ *   min_dist NaN, and it adds nothing to the objective, to any count or to
+ *   any sum.  A centroid with a NaN or infinite coordinate is never chosen
+ *   (it stays empty and keeps its value); a point with no other centroid is
+ *   left unassigned too.  So a Lloyd run from finite centroids keeps them
+ *   finite whatever NaNs the points hold.  kmeans_update skips every idx
+ *   outside [0, K); the points it does sum must be finite.  Finite values
+ *   whose squared norms or products overflow fp32 are outside the contract.
+ *   KNN search takes finite values only.
  * - Ties go to the lowest centroid index.  An empty cluster keeps its previous
  *   centroid (and reports count 0).
  * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
@@ -88,8 +95,10 @@ size_t kmeans_workspace_bytes(int64_t B, int64_t N, int64_t D, int64_t K, int xd
  * centroids, then the arg-min).  The N x K distance matrix is never stored.
  *   X        [B, N, D] xdtype   points (read)
  *   C        [B, K, D] fp32     centroids (read)
- *   idx      [B, N]    int32    written: lowest k minimising ||x - c_k||^2
+ *   idx      [B, N]    int32    written: lowest k minimising ||x - c_k||^2 (-1:
+ *                               unassigned, see non-finite values above)
  *   min_dist [B, N]    fp32     written: that squared distance, clamped at 0
+ *                               (NaN where unassigned)
  */
 int kmeans_assign(const void* X, int xdtype, const float* C, int64_t B, int64_t N, int64_t D,
                   int64_t K, int32_t* idx, float* min_dist, void* ws, size_t ws_bytes,
@@ -121,7 +130,8 @@ int kmeans_update(const void* X, int xdtype, const int32_t* idx, const float* C_
  *   min_dist  [B, N]    fp32   written: distances of the last iteration
  *   counts    [B, K]    int32  written: cluster sizes of the last iteration
  *   objective [B, iters] fp64  written if not NULL: J_t = sum_i min_dist_i of
- *                              the assignment made under C_t, summed in fp64
+ *                              the assignment made under C_t over the assigned
+ *                              points, summed in fp64
  */
 int kmeans_lloyd(const void* X, int xdtype, float* C, int64_t B, int64_t N, int64_t D, int64_t K,
                  int iters, int32_t* idx, float* min_dist, int32_t* counts, double* objective,

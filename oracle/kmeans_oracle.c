@@ -28,6 +28,12 @@
  * cluster keeps its previous centroid; J_t is the objective of the assignment
  * made under C_t, before that iteration's update.
  *
+ * Values that are not finite (the paper does not treat them): a point with a
+ * NaN or infinite coordinate is left unassigned (idx -1, min_dist and gap
+ * NaN); a centroid with one is never chosen, and a point with no centroid
+ * left is unassigned too.  The update counts and sums only points whose idx
+ * is in [0, K); J_t sums the assigned points' min_dist.
+ *
  * KNN search (the same distance with a top-k instead of an arg-min; the paper
  * lists KNN build and search beside KMeans in Section 6 and reports recall
  * 1.0): for query q and database rows r_j,
@@ -80,14 +86,24 @@ int oracle_widen(const void* src, int dtype, int64_t n, double* dst) {
     return ORC_OK;
 }
 
-/* Assignment step for B instances.  gap may be NULL; for K == 1 it is +inf. */
+static int all_finite(const double* v, int64_t n) {
+    for (int64_t j = 0; j < n; ++j)
+        if (!isfinite(v[j])) return 0;
+    return 1;
+}
+
+/* Assignment step for B instances.  gap may be NULL; for K == 1 (one usable
+ * centroid) it is +inf. */
 int oracle_assign(const void* X, int dtype, const double* C, int64_t B, int64_t N,
                   int64_t D, int64_t K, int32_t* idx, double* min_dist, double* gap) {
     if (!X || !C || !idx || !min_dist || !dtype_ok(dtype) || B < 1 || N < 0 || D < 1 || K < 1)
         return ORC_EINVAL;
+    char* usable = (char*)malloc((size_t)K);
+    if (!usable) return ORC_ENOMEM;
     int err = ORC_OK;
     for (int64_t b = 0; b < B; ++b) {
         const double* Cb = C + b * K * D;
+        for (int64_t k = 0; k < K; ++k) usable[k] = (char)all_finite(Cb + k * D, D);
 #pragma omp parallel
         {
             double* x = (double*)malloc((size_t)D * sizeof(double));
@@ -101,15 +117,17 @@ int oracle_assign(const void* X, int dtype, const double* C, int64_t B, int64_t 
                 const int64_t row = b * N + i;
                 for (int64_t j = 0; j < D; ++j) x[j] = widen_one(X, dtype, row * D + j);
                 double best = INFINITY, second = INFINITY;
-                int64_t arg = 0;
-                for (int64_t k = 0; k < K; ++k) {
+                int64_t arg = -1;
+                const int point_ok = all_finite(x, D);
+                for (int64_t k = 0; k < K && point_ok; ++k) {
+                    if (!usable[k]) continue;
                     const double* c = Cb + k * D;
                     double d = 0.0;
                     for (int64_t j = 0; j < D; ++j) {
                         const double t = x[j] - c[j];
                         d += t * t;
                     }
-                    if (d < best) {
+                    if (arg < 0 || d < best) {
                         second = best;
                         best = d;
                         arg = k;
@@ -118,16 +136,18 @@ int oracle_assign(const void* X, int dtype, const double* C, int64_t B, int64_t 
                     }
                 }
                 idx[row] = (int32_t)arg;
-                min_dist[row] = best;
-                if (gap) gap[row] = second - best;
+                min_dist[row] = arg < 0 ? NAN : best;
+                if (gap) gap[row] = arg < 0 ? NAN : second - best;
             }
             free(x);
         }
     }
+    free(usable);
     return err;
 }
 
-/* Update step: per-cluster counts and means; empty clusters keep C_prev. */
+/* Update step: per-cluster counts and means over the points with idx in
+ * [0, K); empty clusters keep C_prev. */
 int oracle_update(const void* X, int dtype, const int32_t* idx, const double* C_prev,
                   int64_t B, int64_t N, int64_t D, int64_t K, double* C_out, int64_t* counts) {
     if (!X || !idx || !C_prev || !C_out || !counts || !dtype_ok(dtype) || B < 1 || N < 0 ||
@@ -143,10 +163,7 @@ int oracle_update(const void* X, int dtype, const int32_t* idx, const double* C_
         for (int64_t i = 0; i < N; ++i) {
             const int64_t row = b * N + i;
             const int32_t k = idx[row];
-            if (k < 0 || k >= K) {
-                err = ORC_EINVAL;
-                break;
-            }
+            if (k < 0 || k >= K) continue;
             n[k] += 1;
             for (int64_t j = 0; j < D; ++j) S[k * D + j] += widen_one(X, dtype, row * D + j);
         }
@@ -179,7 +196,8 @@ int oracle_lloyd(const void* X, int dtype, const double* C0, int64_t B, int64_t 
         if (objective)
             for (int64_t b = 0; b < B; ++b) {
                 double J = 0.0;
-                for (int64_t i = 0; i < N; ++i) J += min_dist[b * N + i];
+                for (int64_t i = 0; i < N; ++i)
+                    if (idx[b * N + i] >= 0) J += min_dist[b * N + i];
                 objective[b * iters + t] = J;
             }
         err = oracle_update(X, dtype, idx, C, B, N, D, K, C_out, counts);

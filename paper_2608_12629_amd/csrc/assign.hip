@@ -173,10 +173,12 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_resident_kernel(
     }
     const int pt = pbase + p * 16 + m;
     if (g == 0 && pt < N) {
+      // unassigned: a norm that is not finite, or no real centroid's score finite
+      const bool asg = xn[p] <= __FLT_MAX__ && v > -__FLT_MAX__;
       const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v, xn[p]), 0.f);
-      idx[pt] = i;
-      min_dist[pt] = md;
-      obj += (double)md;
+      idx[pt] = asg ? i : -1;
+      min_dist[pt] = asg ? md : __builtin_nanf("");
+      obj += asg ? (double)md : 0.0;
     }
   }
 #pragma unroll

@@ -47,6 +47,11 @@ namespace fkm {
 // spread widely subtracts each point's own bound instead (below).
 // Padding rows score -FLT_MAX (an infinity with position bits would be a
 // signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
+// Non-finite values: a centroid with a NaN or infinite coordinate scores NaN
+// or -inf against every point and never wins; a point whose squared norm is
+// not finite, or whose best score is not above -FLT_MAX (no real centroid
+// scored finitely), is left unassigned (idx -1, min_dist NaN, no objective
+// term), and such points do not enter the workgroup's shift.
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -313,8 +318,10 @@ __device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
     for (int c = 0; c < CPL; ++c) ss = chunk_sumsq<DT>(xr[p][c], ss);
     ss += __shfl_xor(ss, 32);
     xn[p] = ss;
-    xmax = __builtin_fmaxf(xmax, ss);
-    xmin = ok ? __builtin_fminf(xmin, ss) : xmin;  // points past N do not count
+    // points past N and points whose norm is not finite (left unassigned) do not count
+    const bool fin = ok && ss <= __FLT_MAX__;
+    xmax = fin ? __builtin_fmaxf(xmax, ss) : xmax;
+    xmin = fin ? __builtin_fminf(xmin, ss) : xmin;
   }
   float Q = 0.f;
   if constexpr (!PPQ) {
@@ -392,10 +399,12 @@ __device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
     i = take ? io : i;
     const int pt = pbase + p * 32 + n;
     if (h == 0 && pt < N) {
+      // unassigned: a norm that is not finite, or no real centroid's score finite
+      const bool asg = xn[p] <= __FLT_MAX__ && v > -__FLT_MAX__;
       const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + (PPQ ? Qp[p] : Q), xn[p]), 0.f);
-      idx[pt] = i;
-      min_dist[pt] = md;
-      obj += (double)md;
+      idx[pt] = asg ? i : -1;
+      min_dist[pt] = asg ? md : __builtin_nanf("");
+      obj += asg ? (double)md : 0.0;
     }
   }
 #pragma unroll

@@ -96,9 +96,13 @@ __device__ __forceinline__ void sk_sums(const uint4 (&xr)[1][CPL], int i, bool o
                                         int* widx, int* lds_cnt, int n, int h, int K, int KT,
                                         f32x16 (&S)[KTM][SkLayout<CPL>::DTL]) {
   constexpr int DTL = SkLayout<CPL>::DTL;
+  // a point outside every cluster enters as zeros (its one-hot column is zero,
+  // and zero times a non-finite coordinate would still be NaN)
+  const bool in = ok && i >= 0 && i < K;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    const uint32_t w[4] = {xr[0][c].x, xr[0][c].y, xr[0][c].z, xr[0][c].w};
+    const uint32_t w[4] = {in ? xr[0][c].x : 0u, in ? xr[0][c].y : 0u, in ? xr[0][c].z : 0u,
+                           in ? xr[0][c].w : 0u};
     const int d0 = (h * CPL + c) * 8;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -107,8 +111,8 @@ __device__ __forceinline__ void sk_sums(const uint4 (&xr)[1][CPL], int i, bool o
     }
   }
   if (h == 0) {
-    widx[n] = ok ? i : -1;
-    if (ok && i >= 0 && i < K) atomicAdd(&lds_cnt[i], 1);
+    widx[n] = in ? i : -1;
+    if (in) atomicAdd(&lds_cnt[i], 1);
   }
   wave_lds_sync();
 #pragma unroll
@@ -245,11 +249,14 @@ __global__ __launch_bounds__(ASSIGN_THREADS, 2) void assign_smallk_kernel(
       const bool take = (vo > v) || (vo == v && io < i);
       v = take ? vo : v;
       i = take ? io : i;
+      // unassigned: a norm that is not finite, or no real centroid's score finite
+      const bool asg = ss <= __FLT_MAX__ && v > -__FLT_MAX__;
+      i = asg ? i : -1;
       if (h == 0) {
         const float md = __builtin_fmaxf(__builtin_fmaf(-2.f, v + Qp[0], ss), 0.f);
         lds_oidx[t * SK_TILE + wave * 32 + n] = i;
-        lds_omd[t * SK_TILE + wave * 32 + n] = md;
-        if (ok) obj += (double)md;
+        lds_omd[t * SK_TILE + wave * 32 + n] = asg ? md : __builtin_nanf("");
+        if (ok && asg) obj += (double)md;
       }
     }
     if constexpr (SUMS) sk_sums<DT, CPL, KTM>(xr, i, ok, xt, widx, lds_cnt, n, h, K, KT, S);

@@ -425,10 +425,12 @@ __global__ __launch_bounds__(256) void decode_keys_kernel(const uint64_t* __rest
   if (i < N) {
     const uint64_t key = keys[(size_t)b * N + i];
     const float v = unordered((uint32_t)(key >> 32));
+    // unassigned: a norm that is not finite, or no real centroid's score finite
+    const bool asg = xn <= __FLT_MAX__ && v > -__FLT_MAX__;
     const float d = __builtin_fmaxf(__builtin_fmaf(-2.f, v + point_q(xn), xn), 0.f);
-    idx[(size_t)b * N + i] = (int32_t)(0xffffffffu - (uint32_t)key);
-    min_dist[(size_t)b * N + i] = d;
-    md = d;
+    idx[(size_t)b * N + i] = asg ? (int32_t)(0xffffffffu - (uint32_t)key) : -1;
+    min_dist[(size_t)b * N + i] = asg ? d : __builtin_nanf("");
+    md = asg ? d : 0.0;
   }
   s[t] = md;
   __syncthreads();

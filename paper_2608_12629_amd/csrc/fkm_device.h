@@ -54,30 +54,36 @@ __device__ inline float chunk_sumsq(const uint4& q, float acc) {
 // One centroid row for the assignment: c^ = round(c) to the storage type
 // into out (D elements) and -|c^|^2 / 2 into *cinit (a padding row: zeros and
 // -FLT_MAX), by one wave: the squares are summed lane-strided and then by a
-// fixed xor butterfly, so wherever this runs the bits are the same.
+// fixed xor butterfly, so wherever this runs the bits are the same.  A row
+// whose |c^|^2 is not finite (a NaN or infinite coordinate) is written as a
+// padding row, so it is never chosen and the kernels' scores stay finite or
+// NaN-free (an infinite score with position bits in its low mantissa would
+// become a signalling NaN in the arg-max tree).
 template <int DT>
 __device__ inline void prep_row(const float* c, bool pad, int D, int lane, void* out,
                                 float* cinit) {
+  auto rounded = [&](int d) -> float {
+    if constexpr (DT == DT_F32) return c[d];
+    else return Elem<DT>::widen(Elem<DT>::narrow(c[d]));
+  };
   float ss = 0.f;
-  if constexpr (DT == DT_F32) {
-    float* o = (float*)out;
+  if (!pad) {
     for (int d = lane; d < D; d += 64) {
-      const float v = pad ? 0.f : c[d];
-      o[d] = v;
-      ss = __builtin_fmaf(v, v, ss);
-    }
-  } else {
-    uint16_t* o = (uint16_t*)out;
-    for (int d = lane; d < D; d += 64) {
-      const uint16_t h = pad ? (uint16_t)0 : Elem<DT>::narrow(c[d]);
-      o[d] = h;
-      const float v = Elem<DT>::widen(h);
+      const float v = rounded(d);
       ss = __builtin_fmaf(v, v, ss);
     }
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
-  if (lane == 0) *cinit = pad ? -0x1.fffffep127f : -0.5f * ss;
+  const bool zero = pad || !(ss <= __FLT_MAX__);  // the same in every lane
+  if constexpr (DT == DT_F32) {
+    float* o = (float*)out;
+    for (int d = lane; d < D; d += 64) o[d] = zero ? 0.f : c[d];
+  } else {
+    uint16_t* o = (uint16_t*)out;
+    for (int d = lane; d < D; d += 64) o[d] = zero ? (uint16_t)0 : Elem<DT>::narrow(c[d]);
+  }
+  if (lane == 0) *cinit = zero ? -0x1.fffffep127f : -0.5f * ss;
 }
 
 // acc += A-chunk x B-chunk over the k-slice these two 16-byte chunks carry.

@@ -354,11 +354,51 @@ def pin_global_minimum(o, seed=15):
         assert abs(best - jstar) <= jstar * Fraction(1, 10 ** 12) + Fraction(1, 10 ** 12)
 
 
+# ------------------------------------------------------------------ non-finite values
+def pin_nonfinite_assign(o):
+    """Hand-worked: a point with a NaN or infinite coordinate is unassigned
+    (idx -1, min_dist and gap NaN); a centroid with one is never chosen, and a
+    finite point with no finite centroid left is unassigned too."""
+    X = _f32([[[0, 0], [np.nan, 1], [np.inf, 0], [3, 0], [-np.inf, 2]]])
+    C = np.array([[[0, 0], [np.nan, 0], [4, 0], [1, np.inf]]])
+    idx, md, gap = o.assign(X, "f32", C)
+    assert idx.tolist() == [[0, -1, -1, 2, -1]]
+    assert md[0, 0] == 0 and md[0, 3] == 1 and np.isnan(md[0, [1, 2, 4]]).all()
+    assert gap[0, 0] == 16 and gap[0, 3] == 8 and np.isnan(gap[0, [1, 2, 4]]).all()
+    # one usable centroid: its distance, and no runner-up (+inf)
+    idx, md, gap = o.assign(_f32([[[1, 1]]]), "f32", np.array([[[np.nan, 0], [0, 0]]]))
+    assert idx.tolist() == [[1]] and md[0, 0] == 2 and gap[0, 0] == np.inf
+    # no usable centroid
+    idx, md, gap = o.assign(_f32([[[1, 1], [2, 2]]]), "f32", np.array([[[np.inf, 0], [0, np.nan]]]))
+    assert idx.tolist() == [[-1, -1]] and np.isnan(md).all()
+    # 16-bit storage: a bf16 NaN and an fp16 infinity read as such
+    for dt, bits in (("bf16", 0x7FC0), ("f16", 0x7C00)):
+        Xb = np.array([[[0, 0], [bits, 0]]], np.uint16)
+        idx, md, _ = o.assign(Xb, dt, np.array([[[0.0, 0.0]]]))
+        assert idx.tolist() == [[0, -1]] and md[0, 0] == 0 and np.isnan(md[0, 1])
+
+
+def pin_nonfinite_update_lloyd(o):
+    """Hand-worked: the update ignores entries outside [0, K); a Lloyd run on
+    points with NaNs leaves them unassigned, keeps every centroid finite and
+    counts only the assigned points in J_t."""
+    X = _f32([[[0, 0], [2, 0], [np.nan, 0], [10, 0], [12, 0]]])
+    C_prev = np.array([[[0.0, 0.0], [10.0, 0.0], [5.0, 5.0]]])
+    C1, n = o.update(X, "f32", np.array([[0, 0, -1, 1, 7]], np.int32), C_prev)
+    assert n.tolist() == [[2, 1, 0]]
+    assert C1[0].tolist() == [[1, 0], [10, 0], [5, 5]]
+    CT, idx, md, n, obj = o.lloyd(X, "f32", C_prev, 2)
+    assert idx.tolist() == [[0, 0, -1, 1, 1]] and n.tolist() == [[2, 2, 0]]
+    assert CT[0].tolist() == [[1, 0], [11, 0], [5, 5]]
+    # J_0 = 0 + 4 + 0 + 4 under C_prev; J_1 = 1 + 1 + 1 + 1 under the means
+    assert obj.tolist() == [[8.0, 4.0]]
+
+
 FAST_PINS = [pin_widen_bf16, pin_widen_f16, pin_exact_dyadic, pin_exact_general, pin_golden_worked,
              pin_scipy_vq, pin_torch_cdist, pin_single_cluster, pin_points_as_centroids,
              pin_duplicate_centroids, pin_1d_midpoints, pin_empty_cluster_kept,
              pin_batched_independent, pin_mass_conservation, pin_fixed_point, pin_blob_recovery,
-             pin_global_minimum]
+             pin_global_minimum, pin_nonfinite_assign, pin_nonfinite_update_lloyd]
 
 
 # ------------------------------------------------------------------ KNN search

@@ -17,7 +17,12 @@ MUTANTS = {
                          "const double t = (j + 1 < D) ? x[j] - c[j] : 0.0;"),
     "sign_flip": ("const double t = x[j] - c[j];", "const double t = x[j] + c[j];"),
     "abs_not_square": ("d += t * t;", "d += fabs(t);"),
-    "tie_to_highest": ("if (d < best) {", "if (d <= best) {"),
+    "tie_to_highest": ("if (arg < 0 || d < best) {", "if (arg < 0 || d <= best) {"),
+    "nonfinite_centroid_used": ("if (!usable[k]) continue;", "(void)usable[k];"),
+    "nonfinite_point_assigned": ("const int point_ok = all_finite(x, D);", "const int point_ok = 1;"),
+    "unassigned_in_objective": ("if (idx[b * N + i] >= 0) J += min_dist[b * N + i];",
+                                "J += min_dist[b * N + i];"),
+    "invalid_idx_ends_instance": ("if (k < 0 || k >= K) continue;", "if (k < 0 || k >= K) break;"),
     "index_off_by_one": ("arg = k;", "arg = k ? k - 1 : 0;"),
     "no_runner_up": ("} else if (d < second) {", "} else if (0) {"),
     "empty_cluster_zeroed": (": prev[j];", ": 0.0;"),
