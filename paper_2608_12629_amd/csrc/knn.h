@@ -335,6 +335,7 @@ hipError_t launch_knn_dt(const void* Q, const void* R, int64_t B, int64_t M, int
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (k <= 8) return launch_knn_k<DT, 8>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
+  if (k <= 10) return launch_knn_k<DT, 10>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
   if (k <= 16) return launch_knn_k<DT, 16>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
   return launch_knn_k<DT, KNN_MAX_K>(Q, chat, cinit, B, M, Np, D, k, nbr_idx, nbr_dist, s);
 }

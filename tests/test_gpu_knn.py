@@ -90,6 +90,7 @@ SHAPES = [
     (1, 500, 5000, 160, 12, "f16"),       # the 16-entry lists in fp16
     (1, 300, 2000, 40, 5, "bf16"),        # D = 40: zero-padded copies to 48
     (2, 200, 1500, 100, 20, "f16"),       # D = 100 -> 112, batched
+    (1, 700, 3000, 128, 9, "f16"),        # the 10-entry lists, two query tiles per wave, fp16
 ]
 
 
