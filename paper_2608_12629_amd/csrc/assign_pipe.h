@@ -37,16 +37,16 @@ namespace fkm {
 // |x|^2/2 over the workgroup's points plus a margin, so every score
 // s' = <x, c^> - |c^|^2/2 - Q is strictly negative and orders the centroids
 // like the distance does.  The lane's position j = 4 q + r is written into the
-// 4 low mantissa bits of each score (one and-or), a max3 tree picks the
-// tile's best (for negative floats larger low bits mean more negative, so on
-// equal upper bits the lowest position wins), and a strict compare on the
-// masked value keeps the earliest tile.  Scores within 16 ulp of each other
+// 4 low mantissa bits of each score (one and-or), an integer min3 tree over
+// the keys picks the tile's best (for negative floats the larger value has
+// the smaller bit pattern, and on equal upper bits the lowest position wins),
+// and a strict compare on the masked value keeps the earliest tile.  Scores within 16 ulp of each other
 // therefore count as ties and go to the lowest index; nothing else changes.
 // Since |s'| is up to about Q, that window (and the error of min_dist) is
 // relative to the workgroup's largest norm; a workgroup whose points' norms
 // spread widely subtracts each point's own bound instead (below).
-// Padding rows score -FLT_MAX (an infinity with position bits would be a
-// signalling NaN); quiet-NaN scores never win (max3 returns the other operand).
+// Padding rows score -FLT_MAX (or -inf once shifted); a NaN key, of either
+// sign, reads as an integer above every finite negative key and never wins.
 // Non-finite values: a centroid with a NaN or infinite coordinate scores NaN
 // or -inf against every point and never wins; a point whose squared norm is
 // not finite, or whose best score is not above -FLT_MAX (no real centroid
@@ -174,26 +174,34 @@ __device__ __forceinline__ void pipe_mfma_tile(f32x16 (&acc)[NSUB], const uint4 
 }
 
 // Packed-key arg-max of one tile into the running (best, code) of each column
-// tile.  PPQ: the scores are shifted here, by each point's own Qp.
+// tile.  PPQ: the scores are shifted here, by each point's own Qp.  Every
+// score is negative: the shift exceeds |x|^2 / 2 by a margin far above the
+// rounding, and padding rows sit at -FLT_MAX (or -inf once shifted).  For
+// negative floats the larger value has the smaller bit pattern read as a
+// signed integer, so the arg-max is an integer minimum over the keys (16
+// distinct keys, the position in the low 4 bits: the lower position wins a
+// tie of the masked scores).  A key made from -inf is a negative NaN; read as
+// an integer it is larger than every finite key, so it never beats a real
+// score.  The integer tree needs none of the NaN quieting a float maximum
+// takes.
 template <int NSUB, bool PPQ>
 __device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_t tcode,
                                               float (&best)[NSUB], uint32_t (&code)[NSUB],
                                               const float (&Qp)[NSUB]) {
 #pragma unroll
   for (int p = 0; p < NSUB; ++p) {
-    float k[16];
+    int k[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j)
-      k[j] = __uint_as_float((__float_as_uint(PPQ ? acc[p][j] - Qp[p] : acc[p][j]) & ~15u) |
-                             (uint32_t)j);
-    const float t0 = __builtin_fmaxf(__builtin_fmaxf(k[0], k[1]), k[2]);
-    const float t1 = __builtin_fmaxf(__builtin_fmaxf(k[3], k[4]), k[5]);
-    const float t2 = __builtin_fmaxf(__builtin_fmaxf(k[6], k[7]), k[8]);
-    const float t3 = __builtin_fmaxf(__builtin_fmaxf(k[9], k[10]), k[11]);
-    const float t4 = __builtin_fmaxf(__builtin_fmaxf(k[12], k[13]), k[14]);
-    const float u0 = __builtin_fmaxf(__builtin_fmaxf(t0, t1), t2);
-    const float u1 = __builtin_fmaxf(__builtin_fmaxf(t3, t4), k[15]);
-    const uint32_t mb = __float_as_uint(__builtin_fmaxf(u0, u1));
+      k[j] = (int)((__float_as_uint(PPQ ? acc[p][j] - Qp[p] : acc[p][j]) & ~15u) | (uint32_t)j);
+    const int t0 = min(min(k[0], k[1]), k[2]);
+    const int t1 = min(min(k[3], k[4]), k[5]);
+    const int t2 = min(min(k[6], k[7]), k[8]);
+    const int t3 = min(min(k[9], k[10]), k[11]);
+    const int t4 = min(min(k[12], k[13]), k[14]);
+    const int u0 = min(min(t0, t1), t2);
+    const int u1 = min(min(t3, t4), k[15]);
+    const uint32_t mb = (uint32_t)min(u0, u1);
     const float mm = __uint_as_float(mb & ~15u);
     const bool gt = mm > best[p];
     best[p] = gt ? mm : best[p];
