@@ -220,11 +220,11 @@ def cpu_baseline(w, sample_rows: int):
             "cpu_model": cpu_model()}
 
 
-def oracle_iteration_seconds(cfg: int) -> float:
-    """One full oracle Lloyd iteration (assignment + update) of workload cfg, in this process."""
+def oracle_iteration_seconds(index: int) -> float:
+    """One full oracle Lloyd iteration (assignment + update) of workload `index`, in this process."""
     from oracle import default
     from paper_2608_12629_amd.synth import make_workload, raw_bits
-    w = make_workload(cfg)
+    w = make_workload(index)
     o = default()
     xr = raw_bits(w.X)
     C64 = w.C0.double().numpy()
@@ -233,7 +233,7 @@ def oracle_iteration_seconds(cfg: int) -> float:
     return time.perf_counter() - t0
 
 
-def single_thread_cfg1():
+def single_thread_small_f32():
     """The fp64 oracle's full Lloyd iteration of the fp32 workload on one host
     thread (a child process with OMP_NUM_THREADS=1; it does not touch the GPU)."""
     env = dict(os.environ, OMP_NUM_THREADS="1")
@@ -572,18 +572,18 @@ def main():
     if not args.no_cpu:
         t0 = time.perf_counter()
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample)
-        st = single_thread_cfg1()
+        st = single_thread_small_f32()
         if st:
-            out["cpu_baseline"]["single_thread_cfg1"] = st
+            out["cpu_baseline"]["single_thread"] = st
         log(f"cpu baseline in {time.perf_counter() - t0:.1f} s")
     if args.extra and args.workload == 3:
         # the other workloads at their own sizes and iteration counts (no cold
         # samples, CPU baseline or ceilings of their own)
         del w
         out["workloads"] = {}
-        for cfg in EXTRA_WORKLOADS:
+        for wl in EXTRA_WORKLOADS:
             t0 = time.perf_counter()
-            wx = make_workload(cfg)
+            wx = make_workload(wl)
             rx = measure(torch, km, wx, wx.iters, args.warmup, args.kernel_reps, args.reps,
                          graph=args.graph)
             fx = fractions(rx, ceil)

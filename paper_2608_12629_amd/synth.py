@@ -158,16 +158,16 @@ def _make_instance(spec: dict, N: int, D: int, K: int, seed_seq: np.random.SeedS
     return labels, centres, rows
 
 
-def make_workload(cfg: int, *, N: Optional[int] = None, K: Optional[int] = None,
+def make_workload(index: int, *, N: Optional[int] = None, K: Optional[int] = None,
                   B: Optional[int] = None, D: Optional[int] = None,
                   n_blobs: Optional[int] = None, seed: Optional[int] = None) -> Workload:
-    """Build workload ``cfg`` (1..6), optionally with smaller sizes.
+    """Build workload ``index`` of WORKLOADS (1..6), optionally with smaller sizes.
 
     Overrides keep the recipe and change only the sizes; ``K`` also sets the
     number of blobs unless ``n_blobs`` is given.  The returned tensors live on
     the CPU.
     """
-    spec = dict(WORKLOADS[cfg])
+    spec = dict(WORKLOADS[index])
     B = B or spec["B"]
     N = N or spec["N"]
     D = D or spec["D"]
@@ -191,8 +191,8 @@ def make_workload(cfg: int, *, N: Optional[int] = None, K: Optional[int] = None,
         if labels is not None:
             labels[b] = lab
             centres.append(cen)
-    name = spec["name"] if (N, K, B, D) == (WORKLOADS[cfg]["N"], WORKLOADS[cfg]["K"],
-                                            WORKLOADS[cfg]["B"], WORKLOADS[cfg]["D"]) \
+    name = spec["name"] if (N, K, B, D) == (WORKLOADS[index]["N"], WORKLOADS[index]["K"],
+                                            WORKLOADS[index]["B"], WORKLOADS[index]["D"]) \
         else f"{spec['name']}@B{B}N{N}D{D}K{K}"
     return Workload(name=name, B=B, N=N, D=D, K=K, dtype=spec["dtype"], iters=spec["iters"],
                     X=X, C0=C0, labels=labels,

@@ -51,18 +51,18 @@ def km():
 
 
 FREE = {
-    "cfg1_full": dict(cfg=1),
-    "cfg2_full": dict(cfg=2),
-    "cfg3_scaled": dict(cfg=3, N=262144, K=1024),
-    "cfg4_full": dict(cfg=4),
-    "cfg5_scaled": dict(cfg=5, N=32768, K=1024),
+    "blobs_f32_full": dict(wl=1),
+    "blobs_1m_bf16_full": dict(wl=2),
+    "zipf_bf16_scaled": dict(wl=3, N=262144, K=1024),
+    "batched_f16_full": dict(wl=4),
+    "subspace_bf16_scaled": dict(wl=5, N=32768, K=1024),
 }
 
 
 @pytest.mark.parametrize("name", list(FREE))
 def test_free_running_lloyd(km, oracle, name):
     kw = dict(FREE[name])
-    w = make_workload(kw.pop("cfg"), **kw)
+    w = make_workload(kw.pop("wl"), **kw)
     T = w.iters
     tol = tol_for(w.dtype)
     say(f"[free {name}] {w.name} B={w.B} N={w.N} D={w.D} K={w.K} {w.dtype} T={T}")

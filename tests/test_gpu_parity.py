@@ -64,34 +64,34 @@ def teacher_forced(km, o, X, C0, dtype, iters, rows=None):
 
 # ----------------------------------------------------------------- workloads
 SMALL = {
-    "cfg1_full": dict(cfg=1),
-    "cfg2_small": dict(cfg=2, N=65536, K=256),
-    "cfg3_small": dict(cfg=3, N=65536, K=512),
-    "cfg4_small": dict(cfg=4, B=8, N=4096),
-    "cfg5_small": dict(cfg=5, N=20000, K=700),
+    "blobs_f32_full": dict(wl=1),
+    "blobs_bf16_small": dict(wl=2, N=65536, K=256),
+    "zipf_bf16_small": dict(wl=3, N=65536, K=512),
+    "batched_f16_small": dict(wl=4, B=8, N=4096),
+    "subspace_bf16_small": dict(wl=5, N=20000, K=700),
 }
 
 
 @pytest.mark.parametrize("name", sorted(SMALL))
 def test_teacher_forced_small(km, oracle, name):
     kw = dict(SMALL[name])
-    w = make_workload(kw.pop("cfg"), **kw)
+    w = make_workload(kw.pop("wl"), **kw)
     say(f"[{name}] {w.name} B={w.B} N={w.N} D={w.D} K={w.K} {w.dtype}")
     teacher_forced(km, oracle, w.X, w.C0, w.dtype, min(w.iters, 4))
 
 
-def test_cfg4_full_teacher_forced(km, oracle):
+def test_batched_f16_full_teacher_forced(km, oracle):
     w = make_workload(4)
-    say(f"[cfg4] {w.name}")
+    say(f"[batched full] {w.name}")
     teacher_forced(km, oracle, w.X, w.C0, w.dtype, 3)
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 5])
-def test_full_size_sampled(km, oracle, cfg):
+@pytest.mark.parametrize("wl", [2, 3, 5], ids=["blobs_1m_bf16", "zipf_8m_bf16", "subspace_2m_d1024_bf16"])
+def test_full_size_sampled(km, oracle, wl):
     """Full-size workload: assignment checked on 4096 sampled rows, update in full."""
-    w = make_workload(cfg)
-    rows = np.sort(np.random.default_rng(cfg).choice(w.N, 4096, replace=False))
-    say(f"[cfg{cfg} full] {w.name}")
+    w = make_workload(wl)
+    rows = np.sort(np.random.default_rng(wl).choice(w.N, 4096, replace=False))
+    say(f"[full] {w.name}")
     teacher_forced(km, oracle, w.X, w.C0, w.dtype, 2, rows=rows)
 
 
@@ -254,9 +254,10 @@ def test_points_as_centroids(km):
 
 
 # ------------------------------------------------------- composition, determinism
-@pytest.mark.parametrize("cfg,kw", [(1, {}), (3, dict(N=65536, K=512)), (4, dict(B=8, N=4096))])
-def test_lloyd_equals_steps_and_is_deterministic(km, oracle, cfg, kw):
-    w = make_workload(cfg, **kw)
+@pytest.mark.parametrize("wl,kw", [(1, {}), (3, dict(N=65536, K=512)), (4, dict(B=8, N=4096))],
+                         ids=["blobs_f32", "zipf_bf16_small", "batched_f16_small"])
+def test_lloyd_equals_steps_and_is_deterministic(km, oracle, wl, kw):
+    w = make_workload(wl, **kw)
     Xd = w.X.cuda()
     iters = 3
     C_a, idx_a, md_a, n_a, obj_a = km.kmeans_lloyd(Xd, w.C0.cuda().clone(), iters)
@@ -330,7 +331,7 @@ def test_fused_lloyd_equals_steps(km, shape):
     assert torch.equal(a[3], n)
 
 
-def test_mass_conservation_full_cfg3(km):
+def test_mass_conservation_full_zipf_8m(km):
     """sum_k n_k c'_k = sum_i x_i at the full 8M-point workload (no oracle needed)."""
     w = make_workload(3)
     Xd = w.X.cuda()

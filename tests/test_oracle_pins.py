@@ -17,16 +17,16 @@ def test_pin_sklearn_lloyd(oracle):
 # Scaled-down versions of the five workloads (same recipe, smaller N/K) for the
 # objective-monotonicity invariant.
 SCALED = [
-    dict(cfg=1, N=8192, K=64),
-    dict(cfg=2, N=8192, K=128),
-    dict(cfg=3, N=16384, K=256),
-    dict(cfg=4, B=4, N=2048),
-    dict(cfg=5, N=2048, K=128),
+    dict(wl=1, N=8192, K=64),
+    dict(wl=2, N=8192, K=128),
+    dict(wl=3, N=16384, K=256),
+    dict(wl=4, B=4, N=2048),
+    dict(wl=5, N=2048, K=128),
 ]
 
 
-@pytest.mark.parametrize("kw", SCALED, ids=lambda kw: f"cfg{kw['cfg']}")
+@pytest.mark.parametrize("kw", SCALED, ids=["blobs_f32", "blobs_bf16", "zipf_bf16", "batched_f16", "subspace_bf16"])
 def test_objective_monotone_on_workloads(oracle, kw):
     kw = dict(kw)
-    w = make_workload(kw.pop("cfg"), **kw)
+    w = make_workload(kw.pop("wl"), **kw)
     P.pin_monotone(oracle, [(w, raw_bits(w.X), w.dtype)])
