@@ -119,17 +119,31 @@ __device__ __forceinline__ T& lds_at(char* base, int lane_off, int imm) {
 }
 
 // Start stage `st` on its way into `buf` (complete after the wave's next
-// vmcnt(0) wait and a barrier) and fetch this thread's score for it.
+// vmcnt(0) wait and a barrier).
 template <int CPL, int LOADS>
-__device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat,
-                                                  const float* __restrict__ cinit, int st, int tid,
-                                                  const PipeOffsets<CPL, LOADS>& o, char* buf) {
+__device__ __forceinline__ void pipe_issue_dma(const u32x4* __restrict__ chat, int st, int tid,
+                                               const PipeOffsets<CPL, LOADS>& o, char* buf) {
   using L = PipeLayout<CPL>;
   const u32x4* src = chat + (size_t)st * L::TCS * L::RC;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
   for (int u = 0; u < LOADS; ++u) lds_dma16(src + o.src[u], buf + (u * ASSIGN_THREADS + wave * 64) * 16);
+}
+
+// This thread's score slot of stage `st`.
+template <int CPL>
+__device__ __forceinline__ float pipe_score(const float* __restrict__ cinit, int st, int tid) {
+  using L = PipeLayout<CPL>;
   return cinit[st * L::TCS + (tid & (L::TCS - 1))];
+}
+
+// Both: the stage's loads, then this thread's score for it.
+template <int CPL, int LOADS>
+__device__ __forceinline__ float pipe_issue_stage(const u32x4* __restrict__ chat,
+                                                  const float* __restrict__ cinit, int st, int tid,
+                                                  const PipeOffsets<CPL, LOADS>& o, char* buf) {
+  pipe_issue_dma<CPL, LOADS>(chat, st, tid, o, buf);
+  return pipe_score<CPL>(cinit, st, tid);
 }
 
 // Rows row0 .. row0 + TCS - 1 of X (rows past N - 1 repeat row N - 1) into
@@ -212,8 +226,15 @@ __device__ __forceinline__ void pipe_epilogue(const f32x16 (&acc)[NSUB], uint32_
 // One stage in `cur`: start the next stage into `nxt`, run the stage's tiles
 // (tile i on one accumulator set beside the epilogue of tile i-1 on the
 // other), store the next stage's scores, then wait for the loads and sync.
+// next = min(st + 1, nst - 1).  `carry` holds this thread's score of stage
+// `next`, fetched one stage earlier: a score fetched in this stage would
+// make the compiler wait for it before the store, and that wait (a vmcnt
+// count) would wait for the stage loads issued before it as well.  The
+// score of the stage after `next` is fetched here instead; the wait at the
+// stage's end covers it.
 template <int DT, int CPL, int NSUB, int LOADS, bool PPQ>
-__device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
+__device__ __forceinline__ void pipe_stage(int st, int next, int nst, float& carry,
+                                           f32x16 (&accA)[NSUB], f32x16 (&accB)[NSUB],
                                            const uint4 (&xr)[NSUB][CPL], char* cur, char* nxt,
                                            const PipeOffsets<CPL, LOADS>& o, const u32x4* chat,
                                            const float* cinit, float Q,
@@ -221,7 +242,9 @@ __device__ __forceinline__ void pipe_stage(int st, int next, f32x16 (&accA)[NSUB
                                            uint32_t& prev_code, float (&best)[NSUB],
                                            uint32_t (&code)[NSUB]) {
   using L = PipeLayout<CPL>;
-  const float nn = pipe_issue_stage<CPL, LOADS>(chat, cinit, next, tid, o, nxt);
+  pipe_issue_dma<CPL, LOADS>(chat, next, tid, o, nxt);
+  const float nn = carry;
+  carry = pipe_score<CPL>(cinit, next + 1 < nst ? next + 1 : nst - 1, tid);
   // issue the prefetch first: left to the scheduler it drifts into the middle
   // of the stage and the wait at the end stalls on it
   __builtin_amdgcn_sched_barrier(0);
@@ -379,19 +402,20 @@ __device__ __forceinline__ void pipe_block(int blk, const uint4* __restrict__ X,
   uint32_t prev_code = 0;
 
   lds_at<float>(buf0, o.n_store, 0) = n0 - Q;
+  float carry = pipe_score<CPL>(cinit, nst > 1 ? 1 : 0, tid);  // the score of stage 1
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int st = 0;
   for (; st + 2 <= nst; st += 2) {   // two stages per trip: each buffer is a fixed array
-    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st + 1, accA, accB, xr, buf0, buf1, o, chat4, cinit,
-                                          Q, Qp, tid, prev_code, best, code);
-    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st + 1, st + 2 < nst ? st + 2 : st + 1, accA, accB, xr,
-                                          buf1, buf0, o, chat4, cinit, Q, Qp, tid, prev_code, best,
-                                          code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st + 1, nst, carry, accA, accB, xr, buf0, buf1, o,
+                                          chat4, cinit, Q, Qp, tid, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st + 1, st + 2 < nst ? st + 2 : st + 1, nst, carry, accA,
+                                          accB, xr, buf1, buf0, o, chat4, cinit, Q, Qp, tid,
+                                          prev_code, best, code);
   }
   if (st < nst)
-    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st, accA, accB, xr, buf0, buf1, o, chat4, cinit, Q,
-                                          Qp, tid, prev_code, best, code);
+    pipe_stage<DT, CPL, NSUB, LOADS, PPQ>(st, st, nst, carry, accA, accB, xr, buf0, buf1, o, chat4,
+                                          cinit, Q, Qp, tid, prev_code, best, code);
   pipe_epilogue<NSUB, PPQ>(accA, prev_code, best, code, Qp);
 
   double obj = 0.0;
