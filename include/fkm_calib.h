@@ -32,8 +32,9 @@ extern "C" {
 int fkm_calib_mfma(float* out, int blocks, int iters, void* stream);
 
 /*
- * Streaming read of `bytes` bytes (a multiple of 16) from `src`, 16 bytes per
- * lane per load, 8 loads in flight.  out [blocks * 256] uint32, written.
+ * Streaming read of `bytes` bytes (a multiple of 16) from `src`: each of the
+ * `blocks` workgroups reads one contiguous range, 16 bytes per lane per load,
+ * 8 non-temporal loads in flight.  out [blocks * 256] uint32, written.
  */
 int fkm_calib_read(const void* src, size_t bytes, uint32_t* out, int blocks, void* stream);
 

@@ -61,19 +61,26 @@ __global__ __launch_bounds__(256, 2) void mfma_loop_kernel(float* __restrict__ o
   out[blockIdx.x * 256 + threadIdx.x] = s;
 }
 
+// Each workgroup streams one contiguous range, 8 loads of 4 KB per workgroup
+// in flight, with the non-temporal hint: on the MI355X this reads ~25% faster
+// than a grid-stride loop of ordinary loads (whose waves touch 8 scattered
+// 1 KB pieces per step), so it is the fairer ceiling for a streaming read.
 __global__ __launch_bounds__(256) void read_kernel(const u32x4* __restrict__ x, size_t n,
                                                    uint32_t* __restrict__ out) {
+  constexpr int U = 8;
   uint32_t acc = 0;
-  const size_t stride = (size_t)gridDim.x * 256;
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  for (; i + 7 * stride < n; i += 8 * stride) {
-    u32x4 v[8];
+  const size_t per = (n + gridDim.x - 1) / gridDim.x;
+  const size_t b0 = (size_t)blockIdx.x * per;
+  const size_t b1 = b0 + per < n ? b0 + per : n;
+  size_t i = b0 + threadIdx.x;
+  for (; i + (U - 1) * 256 < b1; i += U * 256) {
+    u32x4 v[U];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = x[i + u * stride];
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(&x[i + u * 256]);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc ^= v[u][0] + v[u][1] + v[u][2] + v[u][3];
+    for (int u = 0; u < U; ++u) acc ^= v[u][0] + v[u][1] + v[u][2] + v[u][3];
   }
-  for (; i < n; i += stride) {
+  for (; i < b1; i += 256) {
     const u32x4 v = x[i];
     acc ^= v[0] + v[3];
   }
