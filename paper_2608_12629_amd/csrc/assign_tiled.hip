@@ -15,11 +15,13 @@
 // fetches the chunk the swizzled layout puts there).  Four stage buffers let
 // the loads run two to three stages ahead: a barrier without a memory fence
 // (an explicit vmcnt wait for exactly the stage needed next, then s_barrier)
-// keeps the later stages in flight across it.  The buffers are separate LDS
-// arrays and the stage loop is unrolled by four, so the compiler sees that
-// loads in flight into other buffers never alias a stage's reads.  The
-// barrier sits in the middle of a stage: the second 16-dimension step's
+// keeps the later stages in flight across it.  The loads are issued by
+// inline assembly, so the compiler adds no waits of its own for them; the
+// buffers are separate LDS arrays and the stage loop is unrolled by four.
+// The barrier sits in the middle of a stage: the second 16-dimension step's
 // MFMAs run after it, beside the reads of the next stage's first fragments.
+// (One barrier per two stages, with the loads one pair ahead instead of two
+// to three stages, measured 3% slower.)
 //
 // Scores.  The accumulator of point p and centroid c starts at
 // -|c^|^2/2 - Q_p, with Q_p a bound on the point's own |x_p|^2/2 (from a
@@ -73,8 +75,28 @@ static_assert(BP == 256 && BC == 256, "2 x 4 waves of 128 x 64");
 static_assert(2 * LOADS <= 63, "vmcnt counts at most 63 loads");
 static_assert(CB <= TILED_ZERO_BYTES, "a padding stage's centroid chunks fit the zero area");
 
-typedef __attribute__((address_space(1))) void global_void;
-typedef __attribute__((address_space(3))) void lds_void;
+// L2 -> LDS copies of 16 (or 4) bytes per lane into the wave's slots at
+// `lds` (lane l at lds + 16 l, or + 4 l), issued by inline assembly: with the
+// compiler's builtin for them in flight, its own waits around the fragment
+// reads became full drains (vmcnt(0), lgkmcnt(0)) that also waited for the
+// stages loading two and three ahead.  Outside the compiler's view the loads
+// count only in the hardware's in-order vmcnt, which the explicit waits
+// before each barrier govern; M0 (the LDS base) is set in the same statement
+// and used by nothing else in this kernel.
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(base)
+               : "memory");
+}
+__device__ __forceinline__ void dma4(const void* src, char* lds) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(base)
+               : "memory");
+}
 
 // Wait until at most n of this wave's loads are in flight and its LDS
 // accesses are done, then a barrier without a memory fence, so the loads
@@ -136,21 +158,18 @@ __device__ __forceinline__ void tiled_issue(const TiledCtx& c, int s, char* buf)
     const uint32_t off = (c.tid >> 2) + RSTEP * u <= c.last
                              ? c.xoff + u * c.rowsstep
                              : (uint32_t)((c.last * c.RC + ((c.tid & 3) ^ swz(c.tid >> 2))) * 16);
-    __builtin_amdgcn_global_load_lds((global_void*)(xb + off),
-                                     (lds_void*)(buf + (u * TT + wave * 64) * 16), 16, 0, 0);
+    dma16(xb + off, buf + (u * TT + wave * 64) * 16);
   }
   const int krow = (c.cb0 + g) * BC;
   const char* cbp = c.chat + ((size_t)krow * c.RC + ds * CPS) * 16;
 #pragma unroll
   for (int u = 0; u < LC; ++u) {
     const char* src = pad ? c.zero + (u * TT + c.tid) * 16 : cbp + c.coff + u * c.rowsstep;
-    __builtin_amdgcn_global_load_lds((global_void*)src,
-                                     (lds_void*)(buf + XB + (u * TT + wave * 64) * 16), 16, 0, 0);
+    dma16(src, buf + XB + (u * TT + wave * 64) * 16);
   }
   // the block's scores ride with every stage, so every stage issues LOADS loads
   // (waves 4 .. 7 load a second copy, never read)
-  __builtin_amdgcn_global_load_lds((global_void*)(c.cinit + krow + (c.tid & (BC - 1))),
-                                   (lds_void*)(buf + XB + CB + wave * 256), 4, 0, 0);
+  dma4(c.cinit + krow + (c.tid & (BC - 1)), buf + XB + CB + wave * 256);
 }
 
 // Fragments of one 16-dimension step: 4 centroid tiles and 4 point tiles.
