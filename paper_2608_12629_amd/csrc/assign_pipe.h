@@ -63,12 +63,13 @@ typedef __attribute__((address_space(3))) void lds_void;
 // the hardware's in-order vmcnt; the stage ends wait for them explicitly
 // (s_waitcnt vmcnt(0) and a barrier) before any read of that buffer, and the
 // compiler's waits for its own loads stay correct because loads complete in
-// issue order.  M0 (the LDS base) is set here; nothing else in these kernels
-// uses it.
+// issue order.  M0 (the LDS base) is set here, one wait state before the load
+// reads it (the hazard the compiler covers with an s_nop for its own LDS DMA);
+// nothing else in these kernels uses it.
 __device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
   const uint32_t base =
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(src), "s"(base)
                : "memory");

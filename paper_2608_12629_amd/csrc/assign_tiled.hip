@@ -81,18 +81,19 @@ static_assert(CB <= TILED_ZERO_BYTES, "a padding stage's centroid chunks fit the
 // reads became full drains (vmcnt(0), lgkmcnt(0)) that also waited for the
 // stages loading two and three ahead.  Outside the compiler's view the loads
 // count only in the hardware's in-order vmcnt, which the explicit waits
-// before each barrier govern; M0 (the LDS base) is set in the same statement
-// and used by nothing else in this kernel.
+// before each barrier govern; M0 (the LDS base) is set in the same statement,
+// one wait state before the load reads it, and used by nothing else in this
+// kernel.
 __device__ __forceinline__ void dma16(const void* src, char* lds) {
   const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(src), "s"(base)
                : "memory");
 }
 __device__ __forceinline__ void dma4(const void* src, char* lds) {
   const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                :
                : "v"(src), "s"(base)
                : "memory");
