@@ -88,13 +88,21 @@ def _dt(X: torch.Tensor) -> int:
         raise TypeError(f"points must be float32, bfloat16 or float16, got {X.dtype}") from None
 
 
-def _need(t: torch.Tensor, name: str, dtype=None) -> None:
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a GPU tensor")
+def _need(t: torch.Tensor, name: str, dtype=None, numel: Optional[int] = None) -> None:
+    """A contiguous tensor on the current GPU (the library works on the current
+    device); `numel`: the number of elements the kernels read or write there
+    (any shape with that many, so [N] serves for one instance as well as
+    [1, N]).  The C ABI sees pointers only, so these checks are what keeps a
+    kernel inside the tensors it is given."""
+    if not t.is_cuda or t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} must be a tensor on the current GPU (cuda:"
+                         f"{torch.cuda.current_device()}), got {t.device}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements (shape {tuple(t.shape)}), want {numel}")
 
 
 def workspace_bytes(B: int, N: int, D: int, K: int, dtype: torch.dtype) -> int:
@@ -115,6 +123,7 @@ class Workspace:
 def _ws(ws: Optional[Workspace], B, N, D, K, dtype, device) -> Workspace:
     if ws is None or ws.nbytes < workspace_bytes(B, N, D, K, dtype):
         ws = Workspace(B, N, D, K, dtype, device)
+    _need(ws.buf, "workspace", torch.uint8, ws.nbytes)
     return ws
 
 
@@ -126,8 +135,8 @@ def kmeans_assign(X: torch.Tensor, C: torch.Tensor, idx: Optional[torch.Tensor] 
     _need(C, "C", torch.float32)
     idx = torch.empty((B, N), dtype=torch.int32, device=X.device) if idx is None else idx
     min_dist = torch.empty((B, N), dtype=torch.float32, device=X.device) if min_dist is None else min_dist
-    _need(idx, "idx", torch.int32)
-    _need(min_dist, "min_dist", torch.float32)
+    _need(idx, "idx", torch.int32, B * N)
+    _need(min_dist, "min_dist", torch.float32, B * N)
     ws = _ws(ws, B, N, D, K, X.dtype, X.device)
     _check(lib.kmeans_assign(_ptr(X), _dt(X), _ptr(C), B, N, D, K, _ptr(idx), _ptr(min_dist),
                              _ptr(ws.buf), ws.nbytes, _stream()), "kmeans_assign")
@@ -140,12 +149,12 @@ def kmeans_update(X: torch.Tensor, idx: torch.Tensor, C_prev: torch.Tensor,
     """C_out, counts of the centroid update (see ``kmeans_update`` in the header)."""
     B, N, D, K = _shapes(X, C_prev)
     _need(X, "X")
-    _need(idx, "idx", torch.int32)
+    _need(idx, "idx", torch.int32, B * N)
     _need(C_prev, "C_prev", torch.float32)
     C_out = torch.empty((B, K, D), dtype=torch.float32, device=X.device) if C_out is None else C_out
     counts = torch.empty((B, K), dtype=torch.int32, device=X.device) if counts is None else counts
-    _need(C_out, "C_out", torch.float32)
-    _need(counts, "counts", torch.int32)
+    _need(C_out, "C_out", torch.float32, B * K * D)
+    _need(counts, "counts", torch.int32, B * K)
     ws = _ws(ws, B, N, D, K, X.dtype, X.device)
     _check(lib.kmeans_update(_ptr(X), _dt(X), _ptr(idx), _ptr(C_prev), B, N, D, K, _ptr(C_out),
                              _ptr(counts), _ptr(ws.buf), ws.nbytes, _stream()), "kmeans_update")
@@ -177,9 +186,9 @@ def kmeans_lloyd(X: torch.Tensor, C: torch.Tensor, iters: int, *,
             raise ValueError(f"objective has shape {tuple(obj.shape)}, want {(B, iters)}")
     else:
         obj = torch.empty((B, iters), dtype=torch.float64, device=dev) if objective else None
-    for t, name, dt in ((idx, "idx", torch.int32), (min_dist, "min_dist", torch.float32),
-                        (counts, "counts", torch.int32)):
-        _need(t, name, dt)
+    for t, name, dt, n in ((idx, "idx", torch.int32, B * N), (min_dist, "min_dist", torch.float32, B * N),
+                           (counts, "counts", torch.int32, B * K)):
+        _need(t, name, dt, n)
     ws = _ws(ws, B, N, D, K, X.dtype, dev)
     _check(lib.kmeans_lloyd(_ptr(X), _dt(X), _ptr(C), B, N, D, K, int(iters), _ptr(idx),
                             _ptr(min_dist), _ptr(counts), _ptr(obj), _ptr(ws.buf), ws.nbytes,
@@ -235,11 +244,12 @@ def kmeans_knn(Q: torch.Tensor, R: torch.Tensor, k: int, nbr_idx: Optional[torch
     dev = Q.device
     nbr_idx = torch.empty((B, M, k), dtype=torch.int32, device=dev) if nbr_idx is None else nbr_idx
     nbr_dist = torch.empty((B, M, k), dtype=torch.float32, device=dev) if nbr_dist is None else nbr_dist
-    _need(nbr_idx, "nbr_idx", torch.int32)
-    _need(nbr_dist, "nbr_dist", torch.float32)
+    _need(nbr_idx, "nbr_idx", torch.int32, B * M * k)
+    _need(nbr_dist, "nbr_dist", torch.float32, B * M * k)
     need = knn_workspace_bytes(B, M, N, D, k, Q.dtype)
     if ws is None or ws.numel() < need:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _need(ws, "ws", torch.uint8)
     _check(lib.kmeans_knn(_ptr(Q), _ptr(R), _dt(Q), B, M, N, D, int(k), _ptr(nbr_idx),
                           _ptr(nbr_dist), _ptr(ws), ws.numel(), _stream()), "kmeans_knn")
     return nbr_idx, nbr_dist
